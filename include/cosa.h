@@ -1,0 +1,185 @@
+/*
+ * cosa.h — C ABI of the CoSA prefill-attention library for AMD Instinct MI355X (gfx950).
+ *
+ * CoSA ("Accelerating Long-Context Inference via Proxy-Kernel Co-Designed Sparse Attention",
+ * arXiv 2607.25291) computes causal prefill attention in two stages:
+ *   1. the Kernel-Aware Proxy (KAP, Sec. 4.2) scores query-block x key-block importance from
+ *      stride-downsampled Q/K, keeps blocks under a moderate budget and emits, per query block, an
+ *      ordered list of key blocks with the "have rowmax" (HRM) blocks first;
+ *   2. the Ordered-Skipping Kernel (OSK, Sec. 4.3) is a flash-style attention that visits only the
+ *      listed KV pages, in list order, and skips the value side of a block when every row's local
+ *      maximum lies below its running maximum by more than ln(Delta/N) (Eq. (skip)).
+ * Algorithm A (appendix) gives the complete workflow; cosa_prefill runs it end to end.
+ *
+ * Conventions for every entry point
+ *   - Tensors are device pointers (hipMalloc'd or equivalent) owned by the caller; bf16 tensors are
+ *     passed as raw 16-bit storage. Every tensor is dense and contiguous in the layout given.
+ *   - Shapes: Q and O [B, Hq, L, d]; K and V [B, Hkv, L, d]; nb = ceil(L / b).
+ *     Proxy tensors are per KV head: score, hrm, order [B, Hkv, nb, nb]; count [B, Hkv, nb].
+ *     Per-query-head logs: visit_log, margin_log [B, Hq, nb, nb]; n_computed [B, Hq, nb].
+ *   - stream is a hipStream_t (NULL: the legacy default stream). All work is enqueued
+ *     asynchronously on it; nothing is synchronised and nothing is allocated or freed.
+ *   - Arguments are validated on the host before anything is enqueued. On any non-OK status nothing
+ *     has been launched and no output has been written; cosa_last_error() then describes the cause.
+ *     Faults inside kernels surface at the caller's next synchronisation of the stream.
+ *   - Calls on different streams are independent and may run concurrently; the library keeps no
+ *     state between calls apart from the loaded kernels.
+ *   - batch == 0 or seq_len == 0 is an empty problem: the call validates and returns COSA_OK
+ *     without launching anything.
+ *
+ * Supported problem space (COSA_ERR_UNSUPPORTED otherwise): head_dim == 128, block in {64, 128},
+ * causal == 1, seq_len a multiple of block, samples per block (block / stride) in {4, 8, 16, 32},
+ * G * (block / stride) <= 128 rows per proxy unit, and nb <= 8192.
+ */
+#ifndef COSA_H_
+#define COSA_H_
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  COSA_OK = 0,
+  COSA_ERR_INVALID_ARG = 1, /* NULL required pointer, inconsistent shape, value out of range      */
+  COSA_ERR_UNSUPPORTED = 2, /* valid problem outside the supported space listed above             */
+  COSA_ERR_WORKSPACE = 3,   /* workspace NULL or smaller than cosa_prefill_workspace_bytes()       */
+  COSA_ERR_HIP = 4          /* a HIP runtime call or kernel launch failed                         */
+} cosa_status;
+
+/* One attention layer's prefill problem (Algorithm A inputs and parameters). */
+typedef struct {
+  int32_t batch;      /* B >= 0                                                                   */
+  int32_t n_q_heads;  /* Hq >= 1, a multiple of n_kv_heads (grouped-query attention)              */
+  int32_t n_kv_heads; /* Hkv >= 1; query head h reads KV head h / (Hq / Hkv)                       */
+  int32_t seq_len;    /* L = N of the paper >= 0                                                  */
+  int32_t head_dim;   /* d                                                                        */
+  int32_t block;      /* b: query block = key block = KV page, in tokens (appendix: b = 128)      */
+  int32_t stride;     /* s: proxy downsampling stride (Sec. 4.2), divides b; token r*s is sampled  */
+  float sm_scale;     /* logit scale; 0 selects 1/sqrt(head_dim) (Algorithm A)                     */
+  int32_t causal;     /* must be 1 (causal prefill)                                               */
+} cosa_problem;
+
+/* Stage-1 selection (Sec. 4.2 "Flag-grouped sorting", Eq. (mkap)). */
+typedef enum {
+  COSA_SELECT_FRACTION = 0, /* K_i = ceil(value * (i + 1)) of the i + 1 causal candidates,        */
+                            /* clamped to [1, i + 1]; value is taken at 1e-6 resolution            */
+  COSA_SELECT_TOP_P = 1,    /* shortest prefix of the order whose score mass >= value * row total  */
+  COSA_SELECT_ALL = 2       /* every causal candidate (value ignored)                              */
+} cosa_select_mode;
+
+typedef enum {
+  COSA_ORDER_KAP = 0,       /* HRM blocks first, then by descending score; ties by ascending index */
+  COSA_ORDER_ASCENDING = 1  /* the same kept set, listed by ascending block index                  */
+} cosa_order_mode;
+
+typedef struct {
+  cosa_select_mode mode;
+  float value;              /* budget B1 or top-p mass p, in (0, 1] (ignored for ALL)             */
+  cosa_order_mode order;
+} cosa_select;
+
+/* Stage-2 in-kernel skip (Eq. (skip)). */
+typedef enum {
+  COSA_SKIP_NONE = 0,
+  COSA_SKIP_ROWMAX = 1      /* skip a listed block when max_r (m_loc[r] - m[r]) < ln(delta / L)    */
+} cosa_skip_mode;
+
+typedef struct {
+  cosa_skip_mode mode;
+  float delta;              /* skip scale Delta, 0 < delta <= seq_len when mode == ROWMAX          */
+} cosa_skip;
+
+/* Visit codes written to visit_log. */
+#define COSA_VISIT_COMPUTED 1
+#define COSA_VISIT_SKIPPED 2
+
+/* Byte offsets of the proxy tensors inside a cosa_prefill workspace (each 256-byte aligned). */
+typedef struct {
+  size_t score; /* float   [B, Hkv, nb, nb] */
+  size_t hrm;   /* uint8_t [B, Hkv, nb, nb] */
+  size_t order; /* int32_t [B, Hkv, nb, nb] */
+  size_t count; /* int32_t [B, Hkv, nb]     */
+  size_t total; /* bytes required           */
+} cosa_workspace_layout;
+
+/* Human-readable name of a status code (static storage). */
+const char* cosa_status_string(cosa_status status);
+
+/* Detail of the most recent failure in the calling thread ("" if none). Valid until the next
+ * call into the library from the same thread. */
+const char* cosa_last_error(void);
+
+/*
+ * KAP block scoring (Sec. 4.2 "Block ranking", Eq. (score); Algorithm A, proxy stage).
+ * For every batch n, KV head g and query block i, with the sampled rows r = i*spb .. i*spb+spb-1
+ * (spb = b/s, token r*s) of every query head of group g and the sampled keys c <= r (token c*s):
+ *   beta[r, j] = max over the sampled keys c of block j of sm_scale * <Q[r*s], K[c*s]>,
+ *   Pbar[r, j] = exp(beta[r, j] - max_j' beta[r, j'])      (softmax -> MaxPool -> MaxNorm),
+ *   score[n, g, i, j] = sum over the G*spb rows of Pbar[r, j],
+ *   hrm[n, g, i, j]   = 1 if some row attains its maximum in block j, else 0,
+ * for j <= i; entries j > i are not written. fp32 arithmetic on bf16 inputs; the row sum runs in a
+ * fixed order, so results are deterministic.
+ */
+cosa_status cosa_kap_score(const cosa_problem* problem, const void* q, const void* k,
+                           float* score, uint8_t* hrm, void* stream);
+
+/*
+ * Flag-grouped sort and stage-1 cut (Sec. 4.2, Eq. (mkap); Algorithm A, proxy stage).
+ * For every (n, g, i): the candidates j <= i are ordered by (hrm desc, score desc, j asc), the
+ * leading K_i are kept (per select->mode), and order[n, g, i, :] receives them (or the same set by
+ * ascending j for COSA_ORDER_ASCENDING) followed by -1 up to nb; count[n, g, i] = K_i.
+ * Reads score/hrm entries j <= i only.
+ */
+cosa_status cosa_kap_select_ordered(const cosa_problem* problem, const float* score,
+                                    const uint8_t* hrm, const cosa_select* select, int32_t* order,
+                                    int32_t* count, void* stream);
+
+/*
+ * Ordered-skipping attention (Sec. 4.3; Algorithm A, attention loop; Eq. (skip)).
+ * Query head h of batch n and query block i walks order[n, g(h), i, 0 .. count-1] in list order:
+ * S = sm_scale * Q_i K_j^T (causal mask on the diagonal block), m_loc = rowmax(S), running max
+ * m <- max(m, m_loc), margin d = max over the b rows of (m_loc - m) in nats; with
+ * skip->mode == ROWMAX the block's value side is skipped when d < tau, tau = ln(delta / L)
+ * computed in double and rounded once to float. Otherwise the online-softmax state is updated
+ * (P = exp(S - m) rounded to bf16 for the P V product, fp32 accumulation). O = O / l in bf16.
+ * order entries must lie in [0, i] and be distinct; count in [1, nb] (not checked on the device).
+ * skip may be NULL (no skipping). Optional logs (NULL to omit), indexed by list position k:
+ * visit_log (COSA_VISIT_*), margin_log (d in nats), n_computed (computed blocks per tile).
+ */
+cosa_status cosa_osk_attention(const cosa_problem* problem, const void* q, const void* k,
+                               const void* v, const int32_t* order, const int32_t* count,
+                               const cosa_skip* skip, void* o, uint8_t* visit_log,
+                               float* margin_log, int32_t* n_computed, void* stream);
+
+/*
+ * Dense causal flash attention (Sec. 3.1): every key block j <= i in ascending order, same tile
+ * code and numerics as cosa_osk_attention without list and skip. The in-house baseline.
+ */
+cosa_status cosa_dense_attention(const cosa_problem* problem, const void* q, const void* k,
+                                 const void* v, void* o, void* stream);
+
+/* Workspace size of cosa_prefill (0 if the problem is invalid; see cosa_last_error()). */
+size_t cosa_prefill_workspace_bytes(const cosa_problem* problem);
+
+/* Offsets of score/hrm/order/count inside the cosa_prefill workspace. */
+cosa_status cosa_prefill_workspace_layout(const cosa_problem* problem,
+                                          cosa_workspace_layout* layout);
+
+/*
+ * Complete proxy-kernel workflow (Algorithm A): cosa_kap_score, cosa_kap_select_ordered and
+ * cosa_osk_attention enqueued back to back on one stream, with the proxy tensors in the
+ * caller-provided workspace (at least cosa_prefill_workspace_bytes(); contents on return are the
+ * proxy tensors at cosa_prefill_workspace_layout() offsets). skip may be NULL.
+ */
+cosa_status cosa_prefill(const cosa_problem* problem, const void* q, const void* k, const void* v,
+                         const cosa_select* select, const cosa_skip* skip, void* workspace,
+                         size_t workspace_bytes, void* o, void* stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* COSA_H_ */

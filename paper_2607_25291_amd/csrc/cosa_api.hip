@@ -1,0 +1,282 @@
+// C ABI of the CoSA prefill-attention library: host-side validation, workspace layout and launches.
+// Every entry point validates all arguments before enqueuing anything (see include/cosa.h).
+#include <math.h>
+#include <stdarg.h>
+#include <stdio.h>
+
+#include <string>
+
+#include "cosa.h"
+#include "cosa_internal.h"
+
+namespace {
+
+thread_local std::string g_last_error;
+
+cosa_status fail(cosa_status st, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof buf, fmt, ap);
+  va_end(ap);
+  g_last_error = std::string(cosa_status_string(st)) + ": " + buf;
+  return st;
+}
+
+cosa_status ok() {
+  g_last_error.clear();
+  return COSA_OK;
+}
+
+cosa_status hip_fail(hipError_t e, const char* what) {
+  return fail(COSA_ERR_HIP, "%s: %s", what, hipGetErrorString(e));
+}
+
+// Validates the problem and fills the internal shape. `empty` is set for B == 0 or L == 0.
+cosa_status make_shape(const cosa_problem* p, cosa::Shape& sh, bool& empty) {
+  if (!p) return fail(COSA_ERR_INVALID_ARG, "problem is NULL");
+  if (p->batch < 0 || p->seq_len < 0)
+    return fail(COSA_ERR_INVALID_ARG, "batch (%d) and seq_len (%d) must be >= 0", p->batch,
+                p->seq_len);
+  if (p->n_q_heads < 1 || p->n_kv_heads < 1 || p->n_q_heads % p->n_kv_heads != 0)
+    return fail(COSA_ERR_INVALID_ARG, "n_q_heads (%d) must be a positive multiple of n_kv_heads (%d)",
+                p->n_q_heads, p->n_kv_heads);
+  if (p->head_dim < 1 || p->block < 1 || p->stride < 1)
+    return fail(COSA_ERR_INVALID_ARG, "head_dim, block and stride must be >= 1");
+  if (p->block % p->stride != 0)
+    return fail(COSA_ERR_INVALID_ARG, "stride (%d) must divide block (%d)", p->stride, p->block);
+  if (!(p->sm_scale >= 0.f) || !isfinite(p->sm_scale))
+    return fail(COSA_ERR_INVALID_ARG, "sm_scale must be finite and >= 0 (0 = 1/sqrt(d))");
+  if (p->causal != 0 && p->causal != 1)
+    return fail(COSA_ERR_INVALID_ARG, "causal must be 0 or 1");
+  if (p->causal != 1) return fail(COSA_ERR_UNSUPPORTED, "only causal prefill is supported");
+  if (p->head_dim != cosa::kHeadDim)
+    return fail(COSA_ERR_UNSUPPORTED, "head_dim %d (supported: 128)", p->head_dim);
+  if (p->block != 64 && p->block != 128)
+    return fail(COSA_ERR_UNSUPPORTED, "block %d (supported: 64, 128)", p->block);
+  if (p->seq_len % p->block != 0)
+    return fail(COSA_ERR_UNSUPPORTED, "seq_len %d is not a multiple of block %d", p->seq_len,
+                p->block);
+  sh.B = p->batch;
+  sh.Hq = p->n_q_heads;
+  sh.Hkv = p->n_kv_heads;
+  sh.L = p->seq_len;
+  sh.d = p->head_dim;
+  sh.b = p->block;
+  sh.s = p->stride;
+  sh.nb = p->seq_len / p->block;
+  sh.G = p->n_q_heads / p->n_kv_heads;
+  sh.spb = p->block / p->stride;
+  sh.scale = p->sm_scale > 0.f ? p->sm_scale : (float)(1.0 / sqrt((double)p->head_dim));
+  if (sh.nb > 8192) return fail(COSA_ERR_UNSUPPORTED, "%d blocks (supported: <= 8192)", sh.nb);
+  // grid sizes and 32-bit index arithmetic inside the kernels
+  const long long units = (long long)sh.B * sh.Hkv * sh.nb;
+  if (units * sh.G + 8LL * sh.G > (1LL << 30) || (long long)sh.L * cosa::kHeadDim >= (1LL << 31))
+    return fail(COSA_ERR_UNSUPPORTED, "problem too large for one launch");
+  empty = sh.B == 0 || sh.L == 0;
+  return ok();
+}
+
+cosa_status check_proxy_limits(const cosa::Shape& sh) {
+  if (sh.spb != 4 && sh.spb != 8 && sh.spb != 16 && sh.spb != 32)
+    return fail(COSA_ERR_UNSUPPORTED, "block / stride = %d samples per block (supported: 4, 8, 16, 32)",
+                sh.spb);
+  if (sh.G * sh.spb > 128)
+    return fail(COSA_ERR_UNSUPPORTED, "G * samples per block = %d proxy rows (supported: <= 128)",
+                sh.G * sh.spb);
+  if (cosa::kap_score_lds_bytes(sh) == 0)
+    return fail(COSA_ERR_UNSUPPORTED, "proxy block maxima (%d rows x %d blocks) exceed LDS",
+                sh.G * sh.spb, sh.nb);
+  return ok();
+}
+
+cosa_status check_select(const cosa_select* sel, int64_t& micro) {
+  if (!sel) return fail(COSA_ERR_INVALID_ARG, "select is NULL");
+  if (sel->mode != COSA_SELECT_FRACTION && sel->mode != COSA_SELECT_TOP_P &&
+      sel->mode != COSA_SELECT_ALL)
+    return fail(COSA_ERR_INVALID_ARG, "unknown select mode %d", (int)sel->mode);
+  if (sel->order != COSA_ORDER_KAP && sel->order != COSA_ORDER_ASCENDING)
+    return fail(COSA_ERR_INVALID_ARG, "unknown order mode %d", (int)sel->order);
+  micro = 1000000;
+  if (sel->mode != COSA_SELECT_ALL) {
+    if (!(sel->value > 0.f && sel->value <= 1.f))
+      return fail(COSA_ERR_INVALID_ARG, "select value %g outside (0, 1]", (double)sel->value);
+    micro = (int64_t)floor((double)sel->value * 1e6 + 0.5);
+  }
+  return ok();
+}
+
+cosa_status check_skip(const cosa_skip* sk, const cosa::Shape& sh, int& on, float& tau) {
+  on = 0;
+  tau = 0.f;
+  if (!sk || sk->mode == COSA_SKIP_NONE) return ok();
+  if (sk->mode != COSA_SKIP_ROWMAX) return fail(COSA_ERR_INVALID_ARG, "unknown skip mode %d",
+                                                (int)sk->mode);
+  if (!(sk->delta > 0.f) || !isfinite(sk->delta) || (double)sk->delta > (double)sh.L)
+    return fail(COSA_ERR_INVALID_ARG, "skip delta %g outside (0, seq_len = %d]", (double)sk->delta,
+                sh.L);
+  on = 1;
+  tau = (float)log((double)sk->delta / (double)sh.L);  // Eq. (skip): ln(Delta / N)
+  return ok();
+}
+
+size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
+
+cosa_workspace_layout layout_of(const cosa::Shape& sh) {
+  const size_t rows = (size_t)sh.B * sh.Hkv * sh.nb;
+  const size_t cells = rows * sh.nb;
+  cosa_workspace_layout l;
+  l.score = 0;
+  l.hrm = align256(l.score + cells * sizeof(float));
+  l.order = align256(l.hrm + cells * sizeof(uint8_t));
+  l.count = align256(l.order + cells * sizeof(int32_t));
+  l.total = align256(l.count + rows * sizeof(int32_t));
+  return l;
+}
+
+hipStream_t as_stream(void* s) { return reinterpret_cast<hipStream_t>(s); }
+
+}  // namespace
+
+extern "C" {
+
+const char* cosa_status_string(cosa_status status) {
+  switch (status) {
+    case COSA_OK: return "COSA_OK";
+    case COSA_ERR_INVALID_ARG: return "COSA_ERR_INVALID_ARG";
+    case COSA_ERR_UNSUPPORTED: return "COSA_ERR_UNSUPPORTED";
+    case COSA_ERR_WORKSPACE: return "COSA_ERR_WORKSPACE";
+    case COSA_ERR_HIP: return "COSA_ERR_HIP";
+  }
+  return "COSA_ERR_UNKNOWN";
+}
+
+const char* cosa_last_error(void) { return g_last_error.c_str(); }
+
+cosa_status cosa_kap_score(const cosa_problem* problem, const void* q, const void* k, float* score,
+                           uint8_t* hrm, void* stream) {
+  cosa::Shape sh;
+  bool empty = false;
+  cosa_status st = make_shape(problem, sh, empty);
+  if (st != COSA_OK) return st;
+  if (empty) return ok();
+  if ((st = check_proxy_limits(sh)) != COSA_OK) return st;
+  if (!q || !k || !score || !hrm)
+    return fail(COSA_ERR_INVALID_ARG, "q, k, score and hrm must be non-NULL");
+  cosa::KapScoreArgs a{static_cast<const uint16_t*>(q), static_cast<const uint16_t*>(k), score, hrm};
+  const hipError_t e = cosa::launch_kap_score(sh, a, as_stream(stream));
+  return e == hipSuccess ? ok() : hip_fail(e, "kap_score launch");
+}
+
+cosa_status cosa_kap_select_ordered(const cosa_problem* problem, const float* score,
+                                    const uint8_t* hrm, const cosa_select* select, int32_t* order,
+                                    int32_t* count, void* stream) {
+  cosa::Shape sh;
+  bool empty = false;
+  cosa_status st = make_shape(problem, sh, empty);
+  if (st != COSA_OK) return st;
+  int64_t micro = 0;
+  if ((st = check_select(select, micro)) != COSA_OK) return st;
+  if (empty) return ok();
+  if (!score || !hrm || !order || !count)
+    return fail(COSA_ERR_INVALID_ARG, "score, hrm, order and count must be non-NULL");
+  cosa::KapSelectArgs a{score, hrm, order, count, (int)select->mode, (int)select->order, micro};
+  const hipError_t e = cosa::launch_kap_select(sh, a, as_stream(stream));
+  return e == hipSuccess ? ok() : hip_fail(e, "kap_select launch");
+}
+
+cosa_status cosa_osk_attention(const cosa_problem* problem, const void* q, const void* k,
+                               const void* v, const int32_t* order, const int32_t* count,
+                               const cosa_skip* skip, void* o, uint8_t* visit_log,
+                               float* margin_log, int32_t* n_computed, void* stream) {
+  cosa::Shape sh;
+  bool empty = false;
+  cosa_status st = make_shape(problem, sh, empty);
+  if (st != COSA_OK) return st;
+  int on = 0;
+  float tau = 0.f;
+  if ((st = check_skip(skip, sh, on, tau)) != COSA_OK) return st;
+  if (empty) return ok();
+  if (!q || !k || !v || !order || !count || !o)
+    return fail(COSA_ERR_INVALID_ARG, "q, k, v, order, count and o must be non-NULL");
+  cosa::AttnArgs a{static_cast<const uint16_t*>(q), static_cast<const uint16_t*>(k),
+                   static_cast<const uint16_t*>(v), static_cast<uint16_t*>(o), order, count,
+                   visit_log, margin_log, n_computed, on, tau};
+  const hipError_t e = cosa::launch_osk_attention(sh, a, as_stream(stream));
+  return e == hipSuccess ? ok() : hip_fail(e, "osk_attention launch");
+}
+
+cosa_status cosa_dense_attention(const cosa_problem* problem, const void* q, const void* k,
+                                 const void* v, void* o, void* stream) {
+  cosa::Shape sh;
+  bool empty = false;
+  cosa_status st = make_shape(problem, sh, empty);
+  if (st != COSA_OK) return st;
+  if (empty) return ok();
+  if (!q || !k || !v || !o) return fail(COSA_ERR_INVALID_ARG, "q, k, v and o must be non-NULL");
+  cosa::AttnArgs a{static_cast<const uint16_t*>(q), static_cast<const uint16_t*>(k),
+                   static_cast<const uint16_t*>(v), static_cast<uint16_t*>(o), nullptr, nullptr,
+                   nullptr, nullptr, nullptr, 0, 0.f};
+  const hipError_t e = cosa::launch_dense_attention(sh, a, as_stream(stream));
+  return e == hipSuccess ? ok() : hip_fail(e, "dense_attention launch");
+}
+
+cosa_status cosa_prefill_workspace_layout(const cosa_problem* problem,
+                                          cosa_workspace_layout* layout) {
+  cosa::Shape sh;
+  bool empty = false;
+  cosa_status st = make_shape(problem, sh, empty);
+  if (st != COSA_OK) return st;
+  if (!layout) return fail(COSA_ERR_INVALID_ARG, "layout is NULL");
+  *layout = layout_of(sh);
+  return ok();
+}
+
+size_t cosa_prefill_workspace_bytes(const cosa_problem* problem) {
+  cosa_workspace_layout l;
+  if (cosa_prefill_workspace_layout(problem, &l) != COSA_OK) return 0;
+  return l.total;
+}
+
+cosa_status cosa_prefill(const cosa_problem* problem, const void* q, const void* k, const void* v,
+                         const cosa_select* select, const cosa_skip* skip, void* workspace,
+                         size_t workspace_bytes, void* o, void* stream) {
+  cosa::Shape sh;
+  bool empty = false;
+  cosa_status st = make_shape(problem, sh, empty);
+  if (st != COSA_OK) return st;
+  int64_t micro = 0;
+  if ((st = check_select(select, micro)) != COSA_OK) return st;
+  int on = 0;
+  float tau = 0.f;
+  if ((st = check_skip(skip, sh, on, tau)) != COSA_OK) return st;
+  if (empty) return ok();
+  if ((st = check_proxy_limits(sh)) != COSA_OK) return st;
+  if (!q || !k || !v || !o) return fail(COSA_ERR_INVALID_ARG, "q, k, v and o must be non-NULL");
+  const cosa_workspace_layout l = layout_of(sh);
+  if (!workspace || workspace_bytes < l.total)
+    return fail(COSA_ERR_WORKSPACE, "workspace of %zu bytes at %p, need %zu", workspace_bytes,
+                workspace, l.total);
+  char* ws = static_cast<char*>(workspace);
+  float* score = reinterpret_cast<float*>(ws + l.score);
+  uint8_t* hrm = reinterpret_cast<uint8_t*>(ws + l.hrm);
+  int32_t* order = reinterpret_cast<int32_t*>(ws + l.order);
+  int32_t* count = reinterpret_cast<int32_t*>(ws + l.count);
+  const hipStream_t s = as_stream(stream);
+  hipError_t e = cosa::launch_kap_score(
+      sh, cosa::KapScoreArgs{static_cast<const uint16_t*>(q), static_cast<const uint16_t*>(k), score,
+                             hrm},
+      s);
+  if (e != hipSuccess) return hip_fail(e, "kap_score launch");
+  e = cosa::launch_kap_select(
+      sh, cosa::KapSelectArgs{score, hrm, order, count, (int)select->mode, (int)select->order, micro},
+      s);
+  if (e != hipSuccess) return hip_fail(e, "kap_select launch");
+  cosa::AttnArgs a{static_cast<const uint16_t*>(q), static_cast<const uint16_t*>(k),
+                   static_cast<const uint16_t*>(v), static_cast<uint16_t*>(o), order, count,
+                   nullptr, nullptr, nullptr, on, tau};
+  e = cosa::launch_osk_attention(sh, a, s);
+  return e == hipSuccess ? ok() : hip_fail(e, "osk_attention launch");
+}
+
+}  // extern "C"

@@ -1,0 +1,60 @@
+// Internal interface between the C ABI layer (cosa_api.hip) and the kernel translation units.
+// Every launcher enqueues on `stream` and returns the hipError_t of the launch.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+namespace cosa {
+
+constexpr int kHeadDim = 128;
+constexpr int kNumXcd = 8;  // MI355X: 8 accelerator complex dies, workgroups dispatched round-robin
+
+// Shape of one validated problem (all sizes in elements).
+struct Shape {
+  int B, Hq, Hkv, L, d, b, s, nb, G, spb;
+  float scale;  // resolved sm_scale
+};
+
+struct KapScoreArgs {
+  const uint16_t* q;
+  const uint16_t* k;
+  float* score;
+  uint8_t* hrm;
+};
+
+struct KapSelectArgs {
+  const float* score;
+  const uint8_t* hrm;
+  int32_t* order;
+  int32_t* count;
+  int mode;         // cosa_select_mode
+  int order_mode;   // cosa_order_mode
+  int64_t value_micro;  // budget or p in millionths
+};
+
+struct AttnArgs {
+  const uint16_t* q;
+  const uint16_t* k;
+  const uint16_t* v;
+  uint16_t* o;
+  const int32_t* order;   // OSK only
+  const int32_t* count;   // OSK only
+  uint8_t* visit_log;     // optional
+  float* margin_log;      // optional
+  int32_t* n_computed;    // optional
+  int skip_on;
+  float tau;              // skip threshold in nats (float32)
+};
+
+// LDS bytes the proxy-scoring kernel needs for a shape (0 if the shape is outside its limits).
+size_t kap_score_lds_bytes(const Shape& sh);
+size_t kap_select_lds_bytes(const Shape& sh);
+
+hipError_t launch_kap_score(const Shape& sh, const KapScoreArgs& a, hipStream_t stream);
+hipError_t launch_kap_select(const Shape& sh, const KapSelectArgs& a, hipStream_t stream);
+hipError_t launch_osk_attention(const Shape& sh, const AttnArgs& a, hipStream_t stream);
+hipError_t launch_dense_attention(const Shape& sh, const AttnArgs& a, hipStream_t stream);
+
+}  // namespace cosa

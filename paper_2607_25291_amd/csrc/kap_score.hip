@@ -1,0 +1,226 @@
+// KAP block scoring for gfx950 (Sec. 4.2 "Block ranking", Eq. (score); Algorithm A, proxy stage).
+//
+// One workgroup (8 wavefronts) per (batch n, KV head g, query block i). Its R = G * spb sampled query
+// rows (tokens (i*spb + t) * s of the G heads of group g) stay in registers as the MFMA B operand.
+// The waves stride over chunks of 32 sampled keys c < (i+1)*spb (tokens c * s), computing the
+// transposed logits K~ Q~^T with bf16 MFMA 32x32x16, applying sm_scale and the causal mask over
+// sampled positions (c <= r), and reducing them straight into per-block maxima beta[row][j] held in
+// LDS. The softmax -> MaxPool -> MaxNorm chain collapses to Pbar = exp(beta - mu) with mu the row
+// maximum (the softmax normaliser cancels in the MaxNorm ratio, exp is monotone), so the score matrix
+// is never materialised. A second phase takes mu per row and, per key block j, sums
+// exp(beta - mu) over the rows in a fixed order (deterministic) and raises the HRM flag when some
+// row attains its maximum there (beta == mu, exact).
+#include <mutex>
+
+#include "cosa_device.h"
+#include "cosa_internal.h"
+
+namespace cosa {
+namespace {
+
+constexpr int kScoreThreads = 512;
+constexpr int kScoreWaves = kScoreThreads / 64;
+
+struct KapParams {
+  KapScoreArgs a;
+  int Hq, Hkv, L, nb, G, s, R, nbp, n_units;
+  float scale;
+};
+
+template <int SPB, int RT>
+__global__ __launch_bounds__(kScoreThreads) void kap_score_kernel(const KapParams P) {
+  extern __shared__ float beta[];  // [R][nbp]
+  __shared__ float mu[RT * 32];
+
+  const int unit = blockIdx.x;
+  const int i = P.nb - 1 - (unit % P.nb);  // heaviest query blocks first
+  const int ng = unit / P.nb;
+  const int g = ng % P.Hkv, n = ng / P.Hkv;
+  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  const int half = lane >> 5, l32 = lane & 31;
+  const int nkeys = (i + 1) * SPB;
+  const int nchunks = (nkeys + 31) >> 5;
+
+  // Q~^T fragments: row rt*32 + l32 = (head offset hh, sample t) -> token (i*SPB + t) * s.
+  bf16x8_t qf[RT][8];
+#pragma unroll
+  for (int rt = 0; rt < RT; ++rt) {
+    const int row = rt * 32 + l32;
+    if (row < P.R) {
+      const int hh = row / SPB, t = row % SPB;
+      const size_t tok = (size_t)(i * SPB + t) * P.s;
+      const uint16_t* qp =
+          P.a.q + ((size_t)(n * P.Hq + g * P.G + hh) * P.L + tok) * kHeadDim + 8 * half;
+#pragma unroll
+      for (int c = 0; c < 8; ++c) qf[rt][c] = as_bf16x8(ldg16(qp + 16 * c));
+    } else {
+#pragma unroll
+      for (int c = 0; c < 8; ++c) qf[rt][c] = as_bf16x8(u32x4_t{0u, 0u, 0u, 0u});
+    }
+  }
+
+  const uint16_t* kbase = P.a.k + (size_t)ng * P.L * kHeadDim + 8 * half;
+  auto load_keys = [&](int chunk, bf16x8_t (&kf)[8]) {
+    const int c = chunk * 32 + l32;
+    if (chunk < nchunks && c < nkeys) {
+      const uint16_t* kp = kbase + (size_t)c * P.s * kHeadDim;
+#pragma unroll
+      for (int cc = 0; cc < 8; ++cc) kf[cc] = as_bf16x8(ldg16(kp + 16 * cc));
+    } else {
+#pragma unroll
+      for (int cc = 0; cc < 8; ++cc) kf[cc] = as_bf16x8(u32x4_t{0u, 0u, 0u, 0u});
+    }
+  };
+
+  bf16x8_t kcur[8], knext[8];
+  load_keys(w, kcur);
+  for (int chunk = w; chunk < nchunks; chunk += kScoreWaves) {
+    load_keys(chunk + kScoreWaves, knext);  // prefetch
+#pragma unroll
+    for (int rt = 0; rt < RT; ++rt) {
+      f32x16_t acc;
+#pragma unroll
+      for (int r = 0; r < 16; ++r) acc[r] = 0.f;
+#pragma unroll
+      for (int cc = 0; cc < 8; ++cc) acc = mfma32x32x16(kcur[cc], qf[rt][cc], acc);
+      // acc[r]: sampled key chunk*32 + 8 (r/4) + 4 half + r%4, row rt*32 + l32.
+      const int row = rt * 32 + l32;
+      const int rs = i * SPB + (row % SPB);
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int key = chunk * 32 + 8 * (r >> 2) + 4 * half + (r & 3);
+        const float v = acc[r] * P.scale;
+        acc[r] = key > rs ? -INFINITY : v;
+      }
+      const bool row_ok = row < P.R;
+      float* brow = beta + row * P.nbp;
+      if constexpr (SPB == 4) {
+#pragma unroll
+        for (int q4 = 0; q4 < 4; ++q4) {
+          const float bm = fmaxf(fmaxf(acc[4 * q4], acc[4 * q4 + 1]),
+                                 fmaxf(acc[4 * q4 + 2], acc[4 * q4 + 3]));
+          const int j = chunk * 8 + 2 * q4 + half;
+          if (row_ok && j <= i) brow[j] = bm;
+        }
+      } else if constexpr (SPB == 8) {
+#pragma unroll
+        for (int q4 = 0; q4 < 4; ++q4) {
+          float bm = fmaxf(fmaxf(acc[4 * q4], acc[4 * q4 + 1]),
+                           fmaxf(acc[4 * q4 + 2], acc[4 * q4 + 3]));
+          bm = fmaxf(bm, swap_halves(bm));
+          const int j = chunk * 4 + q4;
+          if (row_ok && j <= i && (q4 >> 1) == half) brow[j] = bm;
+        }
+      } else if constexpr (SPB == 16) {
+#pragma unroll
+        for (int b2 = 0; b2 < 2; ++b2) {
+          float bm = acc[8 * b2];
+#pragma unroll
+          for (int r = 1; r < 8; ++r) bm = fmaxf(bm, acc[8 * b2 + r]);
+          bm = fmaxf(bm, swap_halves(bm));
+          const int j = chunk * 2 + b2;
+          if (row_ok && j <= i && b2 == half) brow[j] = bm;
+        }
+      } else {
+        float bm = acc[0];
+#pragma unroll
+        for (int r = 1; r < 16; ++r) bm = fmaxf(bm, acc[r]);
+        bm = fmaxf(bm, swap_halves(bm));
+        const int j = chunk;
+        if (row_ok && j <= i && half == 0) brow[j] = bm;
+      }
+    }
+#pragma unroll
+    for (int cc = 0; cc < 8; ++cc) kcur[cc] = knext[cc];
+  }
+  __syncthreads();
+
+  // Row maxima mu (MaxNorm denominator, in the log domain).
+  for (int row = w; row < P.R; row += kScoreWaves) {
+    float v = -INFINITY;
+    for (int j = lane; j <= i; j += 64) v = fmaxf(v, beta[row * P.nbp + j]);
+    v = wave_max(v);
+    if (lane == 0) mu[row] = v;
+  }
+  __syncthreads();
+
+  float* srow = P.a.score + ((size_t)ng * P.nb + i) * P.nb;
+  uint8_t* hrow = P.a.hrm + ((size_t)ng * P.nb + i) * P.nb;
+  for (int j = tid; j <= i; j += kScoreThreads) {
+    float acc = 0.f;
+    int flag = 0;
+    for (int row = 0; row < P.R; ++row) {
+      const float b = beta[row * P.nbp + j];
+      const float mr = mu[row];
+      acc += expf(b - mr);
+      flag |= (b == mr);
+    }
+    srow[j] = acc;
+    hrow[j] = (uint8_t)flag;
+  }
+}
+
+template <int SPB, int RT>
+hipError_t launch_t(const KapParams& P, size_t lds, hipStream_t stream) {
+  // Dynamic LDS above the default limit has to be allowed per kernel; remember the largest size
+  // granted so far for this instantiation.
+  static std::mutex mu;
+  static size_t granted = 0;
+  if (lds > 48 * 1024) {
+    std::lock_guard<std::mutex> lock(mu);
+    if (lds > granted) {
+      const hipError_t e =
+          hipFuncSetAttribute(reinterpret_cast<const void*>(&kap_score_kernel<SPB, RT>),
+                              hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+      if (e != hipSuccess) return e;
+      granted = lds;
+    }
+  }
+  hipLaunchKernelGGL((kap_score_kernel<SPB, RT>), dim3(P.n_units), dim3(kScoreThreads), lds,
+                     stream, P);
+  return hipGetLastError();
+}
+
+template <int SPB>
+hipError_t launch_spb(const KapParams& P, size_t lds, hipStream_t stream) {
+  const int rt = (P.R + 31) / 32;
+  if (rt <= 1) return launch_t<SPB, 1>(P, lds, stream);
+  if (rt <= 2) return launch_t<SPB, 2>(P, lds, stream);
+  return launch_t<SPB, 4>(P, lds, stream);
+}
+
+}  // namespace
+
+size_t kap_score_lds_bytes(const Shape& sh) {
+  const int R = sh.G * sh.spb;
+  if (R > 128) return 0;
+  if (sh.spb != 4 && sh.spb != 8 && sh.spb != 16 && sh.spb != 32) return 0;
+  const size_t bytes = (size_t)R * (sh.nb + 1) * sizeof(float);
+  // LDS per workgroup on gfx950 is 160 KiB; the static part (mu) needs 512 bytes.
+  if (bytes + 512 > 160 * 1024) return 0;
+  return bytes;
+}
+
+hipError_t launch_kap_score(const Shape& sh, const KapScoreArgs& a, hipStream_t stream) {
+  KapParams P;
+  P.a = a;
+  P.Hq = sh.Hq;
+  P.Hkv = sh.Hkv;
+  P.L = sh.L;
+  P.nb = sh.nb;
+  P.G = sh.G;
+  P.s = sh.s;
+  P.R = sh.G * sh.spb;
+  P.nbp = sh.nb + 1;
+  P.n_units = sh.B * sh.Hkv * sh.nb;
+  P.scale = sh.scale;
+  const size_t lds = kap_score_lds_bytes(sh);
+  switch (sh.spb) {
+    case 4: return launch_spb<4>(P, lds, stream);
+    case 8: return launch_spb<8>(P, lds, stream);
+    case 16: return launch_spb<16>(P, lds, stream);
+    default: return launch_spb<32>(P, lds, stream);
+  }
+}
+
+}  // namespace cosa

@@ -29,6 +29,8 @@ from __future__ import annotations
 
 import dataclasses
 import math
+import os
+from concurrent.futures import ThreadPoolExecutor
 from typing import Optional, Tuple, Union
 
 import numpy as np
@@ -101,11 +103,10 @@ def bf16_bits_to_f32(b: np.ndarray) -> np.ndarray:
 
 def _ar1(rng: np.random.Generator, L: int, d: int, window: int) -> np.ndarray:
     rho = math.exp(-1.0 / window)
-    eps = rng.standard_normal((L, d))
+    x = rng.standard_normal((L, d), dtype=np.float32)
     c0 = math.sqrt(1.0 - rho * rho)
-    x = eps.copy()
-    x[0] = eps[0] / c0                  # so that c[0] = eps[0] (stationary, unit variance)
-    return lfilter([c0], [1.0, -rho], x, axis=0)
+    x[0] /= np.float32(c0)              # so that c[0] = eps[0] (stationary, unit variance)
+    return lfilter(np.array([c0], np.float32), np.array([1.0, -rho], np.float32), x, axis=0)
 
 
 def _unit(rng: np.random.Generator, d: int) -> np.ndarray:
@@ -123,7 +124,7 @@ def make_group(w: Workload, n: int, g: int, seed: Optional[int] = None):
     v = rng.standard_normal((L, d), dtype=np.float32)
     ns = min(w.n_sink, L)
     k[:ns] *= np.float32(w.sink_scale)
-    c = _ar1(rng, L, d, w.window).astype(np.float32)
+    c = _ar1(rng, L, d, w.window)
     q = np.empty((G, L, d), dtype=np.float32)
     for hh in range(G):
         q[hh] = rng.standard_normal((L, d), dtype=np.float32)
@@ -156,12 +157,18 @@ def make_inputs(w: Workload, seed: Optional[int] = None):
     q = np.empty((B, Hq, L, d), dtype=np.uint16)
     k = np.empty((B, Hkv, L, d), dtype=np.uint16)
     v = np.empty((B, Hkv, L, d), dtype=np.uint16)
-    for n in range(B):
-        for g in range(Hkv):
-            qg, kg, vg = make_group(w, n, g, seed)
-            q[n, g * G:(g + 1) * G] = f32_to_bf16_bits(qg)
-            k[n, g] = f32_to_bf16_bits(kg)
-            v[n, g] = f32_to_bf16_bits(vg)
+
+    def one(ng):
+        n, g = divmod(ng, Hkv)
+        qg, kg, vg = make_group(w, n, g, seed)
+        q[n, g * G:(g + 1) * G] = f32_to_bf16_bits(qg)
+        k[n, g] = f32_to_bf16_bits(kg)
+        v[n, g] = f32_to_bf16_bits(vg)
+
+    # groups are independent streams of one seed: generate them concurrently
+    workers = max(1, min(B * Hkv, os.cpu_count() or 1, 16))
+    with ThreadPoolExecutor(max_workers=workers) as ex:
+        list(ex.map(one, range(B * Hkv)))
     return q, k, v
 
 

@@ -1,0 +1,142 @@
+"""Host-side checks of the C ABI that need no GPU: the library loads, exports every function the
+header declares, and rejects invalid arguments before touching the device."""
+import ctypes
+import math
+import os
+import subprocess
+
+import numpy as np
+import pytest
+
+from paper_2607_25291_amd import binding as B
+from paper_2607_25291_amd.calibrate import delta_for_budget
+
+EXPECTED = {"cosa_status_string", "cosa_last_error", "cosa_kap_score", "cosa_kap_select_ordered",
+            "cosa_osk_attention", "cosa_dense_attention", "cosa_prefill_workspace_bytes",
+            "cosa_prefill_workspace_layout", "cosa_prefill"}
+
+
+def test_header_declares_the_abi():
+    assert set(B.declared_symbols()) == EXPECTED
+
+
+def test_library_exports_every_declared_symbol():
+    L = B.lib()
+    for name in B.declared_symbols():
+        assert hasattr(L, name), name
+    out = subprocess.run(["nm", "-D", "--defined-only", B.LIB_PATH], capture_output=True,
+                         text=True, check=True).stdout
+    exported = {line.split()[-1] for line in out.splitlines() if " T " in line}
+    assert EXPECTED <= exported
+
+
+def test_status_strings():
+    names = ["COSA_OK", "COSA_ERR_INVALID_ARG", "COSA_ERR_UNSUPPORTED", "COSA_ERR_WORKSPACE",
+             "COSA_ERR_HIP"]
+    for i, n in enumerate(names):
+        assert B.cosa_status_string(i) == n
+    assert B.cosa_status_string(99) == "COSA_ERR_UNKNOWN"
+
+
+GOOD = B.Problem(1, 8, 2, 1024, 128, 128, 16)
+
+
+@pytest.mark.parametrize("change,status", [
+    (dict(n_q_heads=6, n_kv_heads=4), B.COSA_ERR_INVALID_ARG),
+    (dict(n_kv_heads=0), B.COSA_ERR_INVALID_ARG),
+    (dict(batch=-1), B.COSA_ERR_INVALID_ARG),
+    (dict(stride=24), B.COSA_ERR_INVALID_ARG),
+    (dict(sm_scale=-1.0), B.COSA_ERR_INVALID_ARG),
+    (dict(sm_scale=float("nan")), B.COSA_ERR_INVALID_ARG),
+    (dict(causal=2), B.COSA_ERR_INVALID_ARG),
+    (dict(causal=0), B.COSA_ERR_UNSUPPORTED),
+    (dict(head_dim=64), B.COSA_ERR_UNSUPPORTED),
+    (dict(block=32, stride=4), B.COSA_ERR_UNSUPPORTED),
+    (dict(seq_len=1000), B.COSA_ERR_UNSUPPORTED),
+    (dict(seq_len=128 * 8193), B.COSA_ERR_UNSUPPORTED),
+])
+def test_problem_validation(change, status):
+    p = B.Problem(**{**GOOD.__dict__, **change})
+    with pytest.raises(B.CosaError) as e:
+        B.cosa_dense_attention(p, 16, 16, 16, 16, stream=0)
+    assert e.value.status == status
+    assert B.cosa_status_string(status) in str(e.value)
+
+
+def test_proxy_limits():
+    # 2 samples per block, and too many proxy rows per unit (G * spb > 128)
+    for p in [B.Problem(1, 8, 2, 1024, 128, 128, 64), B.Problem(1, 64, 2, 1024, 128, 128, 16)]:
+        with pytest.raises(B.CosaError) as e:
+            B.cosa_kap_score(p, 16, 16, 16, 16, stream=0)
+        assert e.value.status == B.COSA_ERR_UNSUPPORTED
+        # attention alone does not depend on the proxy limits: it fails only on the NULL pointers
+        with pytest.raises(B.CosaError) as e:
+            B.cosa_dense_attention(p, 16, 16, None, 16, stream=0)
+        assert e.value.status == B.COSA_ERR_INVALID_ARG
+
+
+def test_argument_validation():
+    with pytest.raises(B.CosaError) as e:
+        B.cosa_kap_score(GOOD, 16, None, 16, 16, stream=0)
+    assert e.value.status == B.COSA_ERR_INVALID_ARG
+    for sel in [B.select(B.SELECT_FRACTION, 0.0), B.select(B.SELECT_TOP_P, 1.5),
+                B.select(7, 0.5), B.select(B.SELECT_FRACTION, 0.5, order=5)]:
+        with pytest.raises(B.CosaError) as e:
+            B.cosa_kap_select_ordered(GOOD, 16, 16, sel, 16, 16, stream=0)
+        assert e.value.status == B.COSA_ERR_INVALID_ARG
+    for sk in [B.skip(B.SKIP_ROWMAX, 0.0), B.skip(B.SKIP_ROWMAX, 2000.0),
+               B.skip(B.SKIP_ROWMAX, float("inf")), B.skip(3, 1.0)]:
+        with pytest.raises(B.CosaError) as e:
+            B.cosa_osk_attention(GOOD, 16, 16, 16, 16, 16, sk, 16, stream=0)
+        assert e.value.status == B.COSA_ERR_INVALID_ARG
+    ws = B.cosa_prefill_workspace_bytes(GOOD)
+    with pytest.raises(B.CosaError) as e:
+        B.cosa_prefill(GOOD, 16, 16, 16, B.select(B.SELECT_FRACTION, 0.5), None, 16, ws - 1, 16,
+                       stream=0)
+    assert e.value.status == B.COSA_ERR_WORKSPACE
+    with pytest.raises(B.CosaError) as e:
+        B.cosa_prefill(GOOD, 16, 16, 16, B.select(B.SELECT_FRACTION, 0.5), None, None, ws, 16,
+                       stream=0)
+    assert e.value.status == B.COSA_ERR_WORKSPACE
+
+
+def test_empty_problems_launch_nothing():
+    for p in [B.Problem(0, 8, 2, 1024), B.Problem(1, 8, 2, 0)]:
+        # NULL pointers are fine: nothing is launched
+        B.cosa_dense_attention(p, None, None, None, None, stream=0)
+        B.cosa_kap_score(p, None, None, None, None, stream=0)
+        B.cosa_prefill(p, None, None, None, B.select(B.SELECT_ALL), None, None, 0, None, stream=0)
+        assert B.cosa_last_error() == ""
+
+
+def test_workspace_layout():
+    for (Bt, Hkv, L, b) in [(1, 8, 131072, 128), (2, 2, 2048, 64), (1, 1, 128, 128)]:
+        p = B.Problem(Bt, Hkv * 4, Hkv, L, 128, b, b // 8)
+        lay = B.cosa_prefill_workspace_layout(p)
+        nb = L // b
+        cells = Bt * Hkv * nb * nb
+        al = lambda x: (x + 255) // 256 * 256
+        assert lay.score == 0
+        assert lay.hrm == al(4 * cells)
+        assert lay.order == al(lay.hrm + cells)
+        assert lay.count == al(lay.order + 4 * cells)
+        assert lay.total == al(lay.count + 4 * Bt * Hkv * nb)
+        assert B.cosa_prefill_workspace_bytes(p) == lay.total
+    # 128K, 8 KV heads: 72 MiB
+    assert B.cosa_prefill_workspace_bytes(B.Problem(1, 32, 8, 131072)) == 72 * 2 ** 20 + 32 * 2 ** 10
+
+
+def test_delta_for_budget_host_helper():
+    rng = np.random.default_rng(0)
+    m = np.concatenate([np.zeros(100), -rng.exponential(2.0, 900)])
+    n_causal = 2000
+    delta, k, b = delta_for_budget(m, 1000, n_causal, 0.3, 4096)
+    tau = math.log(delta / 4096)
+    assert k == 400 and (m < tau).sum() == 400 and b == 0.3
+    assert np.min(np.abs(m - tau)) > 0
+    # unreachable: only the 900 negative margins can be skipped
+    delta, k, b = delta_for_budget(m, 1000, n_causal, 0.01, 4096)
+    assert k == 900 and (m < math.log(delta / 4096)).sum() == 900
+    # nothing to skip
+    delta, k, b = delta_for_budget(m, 1000, n_causal, 0.9, 4096)
+    assert k == 0 and (m < math.log(delta / 4096)).sum() == 0
