@@ -213,28 +213,29 @@ def main():
     log(f"[bench] kap_score {t_score:.3f} ms, kap_select {t_select:.3f} ms, osk {t_osk:.3f} ms")
 
     # ---- dense baseline on identical inputs ----
-    B.cosa_dense_attention(p, q, k, v, o_dense)
-    torch.cuda.synchronize()
-    ed = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
-    ed[0].record(stream)
-    for _ in range(args.dense_steps):
+    t_dense = err_max = err_mean = None
+    if args.dense_steps > 0:
         B.cosa_dense_attention(p, q, k, v, o_dense)
-    ed[1].record(stream)
-    torch.cuda.synchronize()
-    t_dense = ed[0].elapsed_time(ed[1]) / args.dense_steps
-    log(f"[bench] dense {t_dense:.3f} ms/layer")
-
-    # output error of KAP+OSK against dense attention (both on the GPU)
-    a = o.view(torch.bfloat16).float()
-    bd = o_dense.view(torch.bfloat16).float()
-    diff = (a - bd).abs()
-    err_max, err_mean = float(diff.max()), float(diff.mean())
-    del a, bd, diff
+        torch.cuda.synchronize()
+        ed = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
+        ed[0].record(stream)
+        for _ in range(args.dense_steps):
+            B.cosa_dense_attention(p, q, k, v, o_dense)
+        ed[1].record(stream)
+        torch.cuda.synchronize()
+        t_dense = ed[0].elapsed_time(ed[1]) / args.dense_steps
+        log(f"[bench] dense {t_dense:.3f} ms/layer")
+        # output error of KAP+OSK against dense attention (both on the GPU)
+        a = o.view(torch.bfloat16).float()
+        bd = o_dense.view(torch.bfloat16).float()
+        diff = (a - bd).abs()
+        err_max, err_mean = float(diff.max()), float(diff.mean())
+        del a, bd, diff
 
     f_osk = osk_flops(cnt_q, ncomp_np, w.block, w.head_dim)
     osk_tflops = f_osk / (t_osk * 1e-3) / 1e12
     f_dense = dense_flops(w.batch, w.n_q_heads, nb, w.block, w.head_dim)
-    dense_tflops = f_dense / (t_dense * 1e-3) / 1e12
+    dense_tflops = f_dense / (t_dense * 1e-3) / 1e12 if t_dense else None
     kf, kb = kap_score_work(w.batch, w.n_q_heads, w.n_kv_heads, nb, w.block, w.stride,
                             w.head_dim)
     traffic = traffic_from_profile("osk_attention", "attention.hip")
@@ -262,9 +263,9 @@ def main():
                    "block": w.block, "stride": w.stride, "kap_budget": w.kap_budget,
                    "osk_budget": w.osk_budget, "select": "fraction", "delta": round(delta, 4),
                    "parallelism": "single GPU"},
-        "speedup_vs_dense": round(t_dense / ms_step, 3),
-        "dense_ms_per_layer": round(t_dense, 3),
-        "dense_tflops": round(dense_tflops, 1),
+        "speedup_vs_dense": round(t_dense / ms_step, 3) if t_dense else None,
+        "dense_ms_per_layer": round(t_dense, 3) if t_dense else None,
+        "dense_tflops": round(dense_tflops, 1) if t_dense else None,
         "stages_ms": {"kap_score": round(t_score, 4), "kap_select": round(t_select, 4),
                       "osk_attention": round(t_osk, 4)},
         "realized_budget": {"stage1": round(b1_real, 5), "overall": round(b_real, 5)},

@@ -28,11 +28,19 @@ struct AttnParams {
   float scale, scale_log2;
 };
 
-template <int BLOCK>
+// HPW query heads of one KV group share a workgroup (and every K/V page staged in its LDS);
+// each head's b-row tile is handled by b/32 wavefronts of 32 rows.
+template <int BLOCK, int HPW>
 struct TileCfg {
-  static constexpr int kWaves = BLOCK / 32;
+  static constexpr int kWavesPerHead = BLOCK / 32;
+  static constexpr int kWaves = HPW * kWavesPerHead;
   static constexpr int kThreads = kWaves * 64;
   static constexpr int kKeyTiles = BLOCK / 32;
+  static constexpr int kKChunks = BLOCK * 16 / kThreads;  // 16-byte K chunks per thread
+  static constexpr int kVGroups = BLOCK * 4 / kThreads;   // (4-key group, 8-wide d slice) per thread
+  static constexpr int kLdsBytes = 2 * 2 * BLOCK * kHeadDim * 2;
+  static constexpr int kWgPerCu = (160 * 1024) / (kLdsBytes + 256);
+  static constexpr int kWavesPerEu = (kWgPerCu * kWaves) / 4 > 1 ? (kWgPerCu * kWaves) / 4 : 1;
 };
 
 template <int BLOCK>
@@ -45,52 +53,59 @@ __device__ __forceinline__ int actual_keygroup(int kq) {
   return (kq & ~3) | ((kq & 1) << 1) | ((kq >> 1) & 1);
 }
 
-// Global -> registers for one K/V page. K: 16-byte chunks, 16 consecutive threads per 256-byte row.
-// V: every thread takes four consecutive keys (one key group) at one 8-wide d slice, so that it can
-// write them transposed; 16 consecutive threads still read whole rows.
-template <int BLOCK>
+// Staging registers for one K/V page on its way from global memory to LDS.
+template <int BLOCK, int HPW>
+struct Stage {
+  u32x4_t k[TileCfg<BLOCK, HPW>::kKChunks];
+  u32x4_t v[TileCfg<BLOCK, HPW>::kVGroups][4];
+};
+
+// K: 16-byte chunks, 16 consecutive threads per 256-byte row. V: every thread takes four
+// consecutive keys (one key group) at one 8-wide d slice so that it can write them transposed;
+// 16 consecutive threads still read whole rows.
+template <int BLOCK, int HPW>
 __device__ __forceinline__ void load_page(const uint16_t* __restrict__ kp,
-                                          const uint16_t* __restrict__ vp, int tid, u32x4_t (&kr)[8],
-                                          u32x4_t (&vr)[8]) {
-  constexpr int NT = TileCfg<BLOCK>::kThreads;
+                                          const uint16_t* __restrict__ vp, int tid,
+                                          Stage<BLOCK, HPW>& st) {
+  using Cfg = TileCfg<BLOCK, HPW>;
 #pragma unroll
-  for (int u = 0; u < 8; ++u) {
-    const int id = u * NT + tid;
-    kr[u] = ldg16(kp + (id >> 4) * kHeadDim + (id & 15) * 8);
+  for (int u = 0; u < Cfg::kKChunks; ++u) {
+    const int id = u * Cfg::kThreads + tid;
+    st.k[u] = ldg16(kp + (id >> 4) * kHeadDim + (id & 15) * 8);
   }
-  const int dg = tid & 15;
 #pragma unroll
-  for (int u2 = 0; u2 < 2; ++u2) {
-    const int kgi = actual_keygroup((tid >> 4) + u2 * (NT / 16));
+  for (int u = 0; u < Cfg::kVGroups; ++u) {
+    const int pi = u * Cfg::kThreads + tid;
+    const int kgi = actual_keygroup(pi >> 4), dg = pi & 15;
 #pragma unroll
-    for (int mm = 0; mm < 4; ++mm) vr[u2 * 4 + mm] = ldg16(vp + (4 * kgi + mm) * kHeadDim + dg * 8);
+    for (int mm = 0; mm < 4; ++mm) st.v[u][mm] = ldg16(vp + (4 * kgi + mm) * kHeadDim + dg * 8);
   }
 }
 
-template <int BLOCK>
-__device__ __forceinline__ void store_k(uint16_t* Ks, const u32x4_t (&kr)[8], int tid) {
-  constexpr int NT = TileCfg<BLOCK>::kThreads;
+template <int BLOCK, int HPW>
+__device__ __forceinline__ void store_k(uint16_t* Ks, const Stage<BLOCK, HPW>& st, int tid) {
+  using Cfg = TileCfg<BLOCK, HPW>;
 #pragma unroll
-  for (int u = 0; u < 8; ++u) {
-    const int id = u * NT + tid;
+  for (int u = 0; u < Cfg::kKChunks; ++u) {
+    const int id = u * Cfg::kThreads + tid;
     const int row = id >> 4, col = id & 15;
-    *reinterpret_cast<u32x4_t*>(Ks + row * kHeadDim + ((col ^ (row & 15)) << 3)) = kr[u];
+    *reinterpret_cast<u32x4_t*>(Ks + row * kHeadDim + ((col ^ (row & 15)) << 3)) = st.k[u];
   }
 }
 
-template <int BLOCK>
-__device__ __forceinline__ void store_vt(uint16_t* Vt, const u32x4_t (&vr)[8], int tid) {
-  constexpr int NT = TileCfg<BLOCK>::kThreads;
-  const int dg = tid & 15;
+template <int BLOCK, int HPW>
+__device__ __forceinline__ void store_vt(uint16_t* Vt, const Stage<BLOCK, HPW>& st, int tid) {
+  using Cfg = TileCfg<BLOCK, HPW>;
 #pragma unroll
-  for (int u2 = 0; u2 < 2; ++u2) {
-    const int kq = (tid >> 4) + u2 * (NT / 16);
+  for (int u = 0; u < Cfg::kVGroups; ++u) {
+    const int pi = u * Cfg::kThreads + tid;
+    const int kq = pi >> 4, dg = pi & 15;
 #pragma unroll
     for (int e = 0; e < 8; ++e) {
       const int d = 8 * dg + e;
       const int wd = e >> 1;
-      const uint32_t k0 = vr[u2 * 4 + 0][wd], k1 = vr[u2 * 4 + 1][wd];
-      const uint32_t k2 = vr[u2 * 4 + 2][wd], k3 = vr[u2 * 4 + 3][wd];
+      const uint32_t k0 = st.v[u][0][wd], k1 = st.v[u][1][wd];
+      const uint32_t k2 = st.v[u][2][wd], k3 = st.v[u][3][wd];
       uint32_t lo, hi;
       if (e & 1) {
         lo = (k0 >> 16) | (k1 & 0xffff0000u);
@@ -105,27 +120,37 @@ __device__ __forceinline__ void store_vt(uint16_t* Vt, const u32x4_t (&vr)[8], i
   }
 }
 
-template <int BLOCK, bool OSK>
-__global__ __launch_bounds__(BLOCK * 2) __attribute__((amdgpu_waves_per_eu(2, 2)))
+// Pipeline over the visited pages (one barrier per page, double-buffered LDS):
+//   prefetch page k+1 into registers | Q K^T of page k (and the tile's skip vote) |
+//   K of page k+1 -> LDS | barrier | skip decision, softmax, P V of page k | V of page k+1 -> LDS.
+// K buffer (k+1)%2 was last read by Q K^T of page k-1 and V buffer (k+1)%2 by P V of page k-1,
+// both finished by every wave before the barrier of page k.
+template <int BLOCK, int HPW, bool OSK>
+__global__ __attribute__((amdgpu_flat_work_group_size(TileCfg<BLOCK, HPW>::kThreads,
+                                                      TileCfg<BLOCK, HPW>::kThreads)))
+__attribute__((amdgpu_waves_per_eu(TileCfg<BLOCK, HPW>::kWavesPerEu,
+                                   TileCfg<BLOCK, HPW>::kWavesPerEu)))
 void attention_kernel(const AttnParams P) {
-  using Cfg = TileCfg<BLOCK>;
+  using Cfg = TileCfg<BLOCK, HPW>;
   constexpr int KT = Cfg::kKeyTiles;
-  __shared__ __attribute__((aligned(16))) uint16_t Ks[BLOCK * kHeadDim];
-  __shared__ __attribute__((aligned(16))) uint16_t Vt[kHeadDim * BLOCK];
-  __shared__ float vote[Cfg::kWaves];
+  constexpr int WPH = Cfg::kWavesPerHead;
+  __shared__ __attribute__((aligned(16))) uint16_t Ks[2][BLOCK * kHeadDim];
+  __shared__ __attribute__((aligned(16))) uint16_t Vt[2][kHeadDim * BLOCK];
+  __shared__ float vote[2][Cfg::kWaves];
 
-  int unit, hh;
-  if (!map_tile(blockIdx.x, P.G, P.n_units, unit, hh)) return;
+  int unit, pair;
+  if (!map_tile(blockIdx.x, P.G / HPW, P.n_units, unit, pair)) return;
   const int i = P.nb - 1 - (unit % P.nb);  // heaviest query blocks first
   const int ng = unit / P.nb;              // n * Hkv + g
   const int g = ng % P.Hkv, n = ng / P.Hkv;
-  const int h = g * P.G + hh;
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
   const int half = lane >> 5, l32 = lane & 31;
+  const int hw = w / WPH, wl = w % WPH;  // head slot in the workgroup, wave within the head
+  const int h = g * P.G + pair * HPW + hw;
 
   const size_t kv_off = (size_t)ng * P.L * kHeadDim;
   const size_t qo_off = (size_t)(n * P.Hq + h) * P.L * kHeadDim;
-  const int qrow = i * BLOCK + w * 32 + l32;
+  const int qrow = i * BLOCK + wl * 32 + l32;
 
   // Q^T as the MFMA B operand: lane owns query row qrow, 8 chunks of 16 d (8 per lane half).
   bf16x8_t qf[8];
@@ -154,36 +179,71 @@ void attention_kernel(const AttnParams P) {
   }
   const size_t log_off = ((size_t)(n * P.Hq + h) * P.nb + i) * P.nb;
   int ncomp = 0;
+  const uint16_t* kbase = P.a.k + kv_off;
+  const uint16_t* vbase = P.a.v + kv_off;
+
+  // A malformed list entry (outside [0, i]) is visited as block i but contributes nothing.
+  auto entry = [&](int kk, bool& valid) -> int {
+    if constexpr (OSK) {
+      const int j = lst[kk];
+      valid = (unsigned)j <= (unsigned)i;
+      return valid ? j : i;
+    } else {
+      valid = true;
+      return kk;
+    }
+  };
+
+  Stage<BLOCK, HPW> st;
+  bool v_cur = false;
+  int j_cur = 0;
+  if (cnt > 0) {
+    j_cur = entry(0, v_cur);
+    load_page<BLOCK, HPW>(kbase + (size_t)j_cur * BLOCK * kHeadDim,
+                          vbase + (size_t)j_cur * BLOCK * kHeadDim, tid, st);
+    store_k<BLOCK, HPW>(Ks[0], st, tid);
+    store_vt<BLOCK, HPW>(Vt[0], st, tid);
+  }
+  __syncthreads();
 
   for (int kk = 0; kk < cnt; ++kk) {
-    const int j = OSK ? lst[kk] : kk;
-    if (OSK && (unsigned)j > (unsigned)i) continue;  // malformed entry: never read out of bounds
-    u32x4_t kr[8], vr[8];
-    load_page<BLOCK>(P.a.k + kv_off + (size_t)j * BLOCK * kHeadDim,
-                     P.a.v + kv_off + (size_t)j * BLOCK * kHeadDim, tid, kr, vr);
-    __syncthreads();  // every wave is done with the previous page
-    store_k<BLOCK>(Ks, kr, tid);
-    store_vt<BLOCK>(Vt, vr, tid);
-    __syncthreads();
+    const int buf = kk & 1;
+    const bool has_next = kk + 1 < cnt;
+    bool v_next = false;
+    int j_next = 0;
+    int tx = tid;  // per-thread copy offsets, recomputed each page (see lx below)
+    asm volatile("" : "+v"(tx));
+    if (has_next) {
+      j_next = entry(kk + 1, v_next);
+      load_page<BLOCK, HPW>(kbase + (size_t)j_next * BLOCK * kHeadDim,
+                            vbase + (size_t)j_next * BLOCK * kHeadDim, tx, st);
+    }
 
+    // The swizzled LDS offsets are cheap to recompute; keeping them out of loop-invariant code
+    // motion saves ~40 registers that would otherwise stay live across the whole page loop.
+    int lx = l32;
+    asm volatile("" : "+v"(lx));
     // S^T tile t: keys 32 t + 8 (r / 4) + 4 half + r % 4 (register r) of query row qrow.
     f32x16_t s[KT];
+    float mnew = m;
+    const uint16_t* Kb = Ks[buf];
 #pragma unroll
     for (int t = 0; t < KT; ++t) {
-      const int key = 32 * t + l32;
+      const int key = 32 * t + lx;
       f32x16_t acc;
 #pragma unroll
       for (int r = 0; r < 16; ++r) acc[r] = 0.f;
 #pragma unroll
       for (int c = 0; c < 8; ++c) {
         const bf16x8_t kf = as_bf16x8(*reinterpret_cast<const u32x4_t*>(
-            Ks + key * kHeadDim + (((2 * c + half) ^ (key & 15)) << 3)));
+            Kb + key * kHeadDim + (((2 * c + half) ^ (lx & 15)) << 3)));
         acc = mfma32x32x16(kf, qf[c], acc);
       }
       s[t] = acc;
+      __builtin_amdgcn_sched_barrier(0);  // bound the live fragments to one key tile
     }
-    if (j == i) {  // diagonal block: causal mask inside the tile
-      const int qi = w * 32 + l32;
+    if (j_cur == i) {  // diagonal block: causal mask inside the tile
+      const int qi = wl * 32 + l32;
 #pragma unroll
       for (int t = 0; t < KT; ++t)
 #pragma unroll
@@ -198,21 +258,26 @@ void attention_kernel(const AttnParams P) {
 #pragma unroll
       for (int r = 0; r < 16; ++r) mloc = fmaxf(mloc, s[t][r]);
     mloc = fmaxf(mloc, swap_halves(mloc));
-    const float mnew = fmaxf(m, mloc);
-
-    bool skip = false;
+    if (v_cur) mnew = fmaxf(m, mloc);
     if constexpr (OSK) {
-      // Eq. (skip): the tile votes with the largest (m_loc - m) over its b rows, in nats.
+      // Eq. (skip): each head's b-row tile votes with its largest (m_loc - m), in nats.
       const float marg = wave_max((mloc - mnew) * P.scale);
-      if (lane == 0) vote[w] = marg;
-      __syncthreads();
-      float dk = vote[0];
+      if (lane == 0) vote[buf][w] = marg;
+    }
+    if (has_next) store_k<BLOCK, HPW>(Ks[buf ^ 1], st, tx);
+    __syncthreads();
+
+    bool skip = !v_cur;
+    if constexpr (OSK) {
+      if (v_cur) {
+        float dk = vote[buf][hw * WPH];
 #pragma unroll
-      for (int ww = 1; ww < Cfg::kWaves; ++ww) dk = fmaxf(dk, vote[ww]);
-      skip = P.a.skip_on && (dk < P.a.tau);
-      if (tid == 0) {
-        if (P.a.visit_log) P.a.visit_log[log_off + kk] = skip ? 2 : 1;
-        if (P.a.margin_log) P.a.margin_log[log_off + kk] = dk;
+        for (int ww = 1; ww < WPH; ++ww) dk = fmaxf(dk, vote[buf][hw * WPH + ww]);
+        skip = P.a.skip_on && (dk < P.a.tau);
+        if (wl == 0 && lane == 0) {
+          if (P.a.visit_log) P.a.visit_log[log_off + kk] = skip ? 2 : 1;
+          if (P.a.margin_log) P.a.margin_log[log_off + kk] = dk;
+        }
       }
     }
     // A skip implies m_loc < m in every row, so the running max is unchanged either way.
@@ -235,6 +300,7 @@ void attention_kernel(const AttnParams P) {
 #pragma unroll
         for (int r = 0; r < 16; ++r) o[dt][r] *= alpha;
       // O^T += V^T P^T over 16-key chunks kc; P^T chunk kc = registers 8 (kc % 2) .. +7 of tile kc / 2.
+      const uint16_t* Vb = Vt[buf];
 #pragma unroll
       for (int kc = 0; kc < BLOCK / 16; ++kc) {
         bf16x8_t pf;
@@ -242,15 +308,23 @@ void attention_kernel(const AttnParams P) {
         for (int e = 0; e < 8; ++e) pf[e] = (__bf16)s[kc >> 1][8 * (kc & 1) + e];
 #pragma unroll
         for (int dt = 0; dt < 4; ++dt) {
-          const int d = 32 * dt + l32;
+          const int d = 32 * dt + lx;
           const int u = (4 * kc + 2 * half) ^ (2 * vt_swizzle<BLOCK>(d));
           const bf16x8_t vf =
-              as_bf16x8(*reinterpret_cast<const u32x4_t*>(Vt + d * BLOCK + u * 4));
+              as_bf16x8(*reinterpret_cast<const u32x4_t*>(Vb + d * BLOCK + u * 4));
           o[dt] = mfma32x32x16(vf, pf, o[dt]);
         }
+        if (kc & 1) __builtin_amdgcn_sched_barrier(0);  // and to two 16-key chunks of V
       }
       ++ncomp;
     }
+    if (has_next) {
+      int ty = tid;
+      asm volatile("" : "+v"(ty));
+      store_vt<BLOCK, HPW>(Vt[buf ^ 1], st, ty);
+    }
+    j_cur = j_next;
+    v_cur = v_next;
   }
 
   lsum += swap_halves(lsum);
@@ -272,8 +346,17 @@ void attention_kernel(const AttnParams P) {
       *reinterpret_cast<u32x2_t*>(op + d0) = u32x2_t{wv[0], wv[1]};
     }
   if constexpr (OSK) {
-    if (tid == 0 && P.a.n_computed) P.a.n_computed[(size_t)(n * P.Hq + h) * P.nb + i] = ncomp;
+    if (wl == 0 && lane == 0 && P.a.n_computed)
+      P.a.n_computed[(size_t)(n * P.Hq + h) * P.nb + i] = ncomp;
   }
+}
+
+template <int BLOCK, int HPW, bool OSK>
+void launch_t(const AttnParams& P, int G, hipStream_t stream) {
+  using Cfg = TileCfg<BLOCK, HPW>;
+  const int slots = (P.n_units + kNumXcd - 1) / kNumXcd * kNumXcd * (G / HPW);
+  hipLaunchKernelGGL((attention_kernel<BLOCK, HPW, OSK>), dim3(slots), dim3(Cfg::kThreads), 0,
+                     stream, P);
 }
 
 template <bool OSK>
@@ -288,11 +371,13 @@ hipError_t launch(const Shape& sh, const AttnArgs& a, hipStream_t stream) {
   P.n_units = sh.B * sh.Hkv * sh.nb;
   P.scale = sh.scale;
   P.scale_log2 = sh.scale * 1.4426950408889634f;
-  const int slots = (P.n_units + kNumXcd - 1) / kNumXcd * kNumXcd * sh.G;
+  const bool pair = (sh.G % 2) == 0;
   if (sh.b == 128) {
-    hipLaunchKernelGGL((attention_kernel<128, OSK>), dim3(slots), dim3(256), 0, stream, P);
+    if (pair) launch_t<128, 2, OSK>(P, sh.G, stream);
+    else launch_t<128, 1, OSK>(P, sh.G, stream);
   } else {
-    hipLaunchKernelGGL((attention_kernel<64, OSK>), dim3(slots), dim3(128), 0, stream, P);
+    if (pair) launch_t<64, 2, OSK>(P, sh.G, stream);
+    else launch_t<64, 1, OSK>(P, sh.G, stream);
   }
   return hipGetLastError();
 }
