@@ -72,8 +72,12 @@ def traffic_from_profile(kernel_tag: str, src: str):
     return rec.get("bytes_per_launch")
 
 
-def cpu_baseline(w, q, k, v, gpu_count, gpu_ncomp, delta, budget_s: float = 20.0):
-    """Time the oracle (as it stands) on sampled units of the same workload, scaled to ms/layer."""
+def cpu_baseline(w, q, k, v, gpu_count, gpu_ncomp, delta, budget_s: float = 15.0):
+    """Time the oracle (as it stands) on sampled units of the same workload, scaled to ms/layer.
+
+    Units are drawn in rounds (query blocks spread over the causal range, two KV heads / two query
+    heads) until about budget_s seconds of oracle work have been timed.
+    """
     from oracle import cosa_oracle as O
     try:
         from threadpoolctl import threadpool_info
@@ -81,30 +85,38 @@ def cpu_baseline(w, q, k, v, gpu_count, gpu_ncomp, delta, budget_s: float = 20.0
     except Exception:  # pragma: no cover
         cores = os.cpu_count() or 1
     nb, G = w.n_blocks, w.n_q_heads // w.n_kv_heads
-    blocks = sorted(set(np.linspace(0, nb - 1, 6).round().astype(int).tolist()))
-    kv_units = [(0, g, i) for g in (0, w.n_kv_heads - 1) for i in blocks]
-    q_units = [(0, h, i) for h in (0, w.n_q_heads - 1) for i in blocks]
-    t0 = time.perf_counter()
-    sc, hr = O.kap_score(q, k, n_kv_heads=w.n_kv_heads, block=w.block, stride=w.stride,
-                         units=kv_units)
-    order, count = O.kap_select(sc, hr, mode=O.SELECT_FRACTION, value=w.kap_budget,
-                                units=kv_units)
-    t_kap = time.perf_counter() - t0
-    t0 = time.perf_counter()
-    r = O.osk_attention(q, k, v, order, count, block=w.block, skip_mode=O.SKIP_ROWMAX,
-                        delta=delta, units=q_units)
-    t_osk = time.perf_counter() - t0
+    rng = np.random.default_rng(1)
+    t_kap = t_osk = 0.0
+    kap_smp = osk_smp = 0.0
+    n_kv = n_q = 0
+    while t_kap + t_osk < budget_s and n_kv < 4 * nb:
+        blocks = sorted(rng.choice(nb, size=min(8, nb), replace=False).tolist())
+        kv_units = [(0, g, i) for g in (0, w.n_kv_heads - 1) for i in blocks]
+        q_units = [(0, h, i) for h in (0, w.n_q_heads - 1) for i in blocks]
+        t0 = time.perf_counter()
+        sc, hr = O.kap_score(q, k, n_kv_heads=w.n_kv_heads, block=w.block, stride=w.stride,
+                             units=kv_units)
+        order, count = O.kap_select(sc, hr, mode=O.SELECT_FRACTION, value=w.kap_budget,
+                                    units=kv_units)
+        t_kap += time.perf_counter() - t0
+        t0 = time.perf_counter()
+        r = O.osk_attention(q, k, v, order, count, block=w.block, skip_mode=O.SKIP_ROWMAX,
+                            delta=delta, units=q_units)
+        t_osk += time.perf_counter() - t0
+        kap_smp += sum(i + 1 for (_, _, i) in kv_units)
+        osk_smp += sum(int(count[n, h // G, i]) + r["n_computed"][(n, h, i)]
+                       for (n, h, i) in q_units)
+        n_kv += len(kv_units)
+        n_q += len(q_units)
     # causal cost model: proxy unit ~ (i+1) keys; OSK tile ~ listed + computed blocks
     kap_all = w.batch * w.n_kv_heads * nb * (nb + 1) / 2
-    kap_smp = sum(i + 1 for (_, _, i) in kv_units)
     osk_all = float(np.repeat(gpu_count, G, axis=1).sum() + gpu_ncomp.sum())
-    osk_smp = sum(int(count[n, h // G, i]) + r["n_computed"][(n, h, i)] for (n, h, i) in q_units)
     est_s = t_kap * kap_all / kap_smp + t_osk * osk_all / max(osk_smp, 1)
     return {"value": est_s * 1e3, "unit": "ms/layer", "cores": int(cores), "kind": "oracle",
-            "sample": (f"{len(kv_units)} proxy units (2 KV heads x {len(blocks)} query blocks) and "
-                       f"{len(q_units)} OSK tiles (2 query heads x {len(blocks)} query blocks) of "
-                       f"the same inputs, {t_kap + t_osk:.1f} s, scaled by the causal cost model "
-                       "(proxy ~ i+1, OSK ~ listed + computed blocks)")}
+            "sample": (f"{n_kv} proxy units (2 KV heads x random query blocks) and {n_q} OSK "
+                       f"tiles (2 query heads x the same query blocks) of the same inputs, "
+                       f"{t_kap + t_osk:.1f} s of oracle time, scaled to one layer by the causal "
+                       "cost model (proxy unit ~ i+1 keys, OSK tile ~ listed + computed blocks)")}
 
 
 def main():

@@ -1,21 +1,29 @@
 // Ordered-skipping attention (OSK) and the dense causal flash baseline for gfx950.
 //
-// One workgroup computes one (query head, query block) tile of b rows: b/32 wavefronts, 32 query
-// rows each. Per visited key block j the K and V pages are staged through LDS, the logits are formed
-// transposed, S^T = K Q^T, with bf16 MFMA 32x32x16 so that every lane owns one query row, and the
-// online softmax runs in fp32 (Sec. 3.1). OSK walks the KAP list (Algorithm A, attention loop) and
-// after Q K^T decides, for the whole b-row tile at once, whether the value side can be skipped
+// A workgroup computes HPW query heads of one KV group for one query block of b rows: b/32
+// wavefronts per head, 32 query rows per wavefront. The K and V pages of each visited key block are
+// staged through LDS once and serve every head of the workgroup. Logits are formed transposed,
+// S^T = K Q^T, with bf16 MFMA 32x32x16 so that every lane owns one query row; the online softmax
+// runs in fp32 (Sec. 3.1). OSK walks the KAP list (Algorithm A, attention loop) and after Q K^T
+// decides, for each head's whole b-row tile at once, whether the value side can be skipped
 // (Eq. (skip)); the dense kernel visits j = 0..i in order and never skips.
 //
-// LDS layouts (b = 128 shown; bank model 64 x 4 B):
-//   Ks[key][d]   row-major, the 16-byte chunk c of row `key` stored at chunk c ^ (key % 16):
-//                conflict-free both for the coalesced row writes and for the MFMA A-operand reads
-//                (lane = key, 16 bytes of d).
-//   Vt[d][key']  V transposed, so that the P V MFMA reads eight keys of one d as 16 bytes. Keys are
-//                permuted inside every 16 (swap of offset bits 2 and 3) so that those eight keys are
-//                exactly the eight the lane holds in P^T (see the S^T register layout), and 8-byte
-//                units are XOR-swizzled with 2 * ((d % 16) ^ (d / 16 % 8)) so that both the
-//                transposing 8-byte writes and the 16-byte reads are conflict-free.
+// Pipeline (double-buffered LDS, one barrier per page): the next page's global loads are issued
+// into registers, Q K^T of the current page runs (and each wave posts its skip-vote value), the
+// next K page goes to LDS, barrier, the tile decides, softmax and P V run, the next V page goes to
+// LDS. K buffer (k+1)%2 was last read by Q K^T of page k-1 and V buffer (k+1)%2 by P V of page k-1,
+// both finished by every wave before the barrier of page k.
+//
+// LDS layouts (64 banks x 4 bytes; rows padded by 16 bytes so that 16 consecutive rows start in 16
+// different 4-bank groups):
+//   K  [key][d]  row-major, 272-byte rows. MFMA A-operand reads (lane = key, 16 bytes of d) and the
+//                coalesced row writes are conflict-free; read addresses are one base register plus
+//                immediates.
+//   Vt [d][key'] V transposed, so that the P V MFMA reads eight keys of one d as 16 bytes. Keys are
+//                permuted inside every 16 (offset bits 2 and 3 swapped) so that those eight keys are
+//                the eight the lane holds in P^T. Row d is stored at row slot d ^ ((d / 16) % 8), which
+//                keeps both the 16-byte reads (16 consecutive d) and the transposing 8-byte writes
+//                (d = 8 g + e for 16 values of g) conflict-free.
 #include "cosa_device.h"
 #include "cosa_internal.h"
 
@@ -28,8 +36,6 @@ struct AttnParams {
   float scale, scale_log2;
 };
 
-// HPW query heads of one KV group share a workgroup (and every K/V page staged in its LDS);
-// each head's b-row tile is handled by b/32 wavefronts of 32 rows.
 template <int BLOCK, int HPW>
 struct TileCfg {
   static constexpr int kWavesPerHead = BLOCK / 32;
@@ -38,71 +44,90 @@ struct TileCfg {
   static constexpr int kKeyTiles = BLOCK / 32;
   static constexpr int kKChunks = BLOCK * 16 / kThreads;  // 16-byte K chunks per thread
   static constexpr int kVGroups = BLOCK * 4 / kThreads;   // (4-key group, 8-wide d slice) per thread
-  static constexpr int kLdsBytes = 2 * 2 * BLOCK * kHeadDim * 2;
+  static constexpr int kKRow = (kHeadDim + 8) * 2;        // bytes per K row in LDS
+  static constexpr int kVRow = (BLOCK + 8) * 2;           // bytes per V^T row in LDS
+  static constexpr int kKBytes = BLOCK * kKRow;
+  static constexpr int kVBytes = kHeadDim * kVRow;
+  static constexpr int kLdsBytes = 2 * (kKBytes + kVBytes);
   static constexpr int kWgPerCu = (160 * 1024) / (kLdsBytes + 256);
   static constexpr int kWavesPerEu = (kWgPerCu * kWaves) / 4 > 1 ? (kWgPerCu * kWaves) / 4 : 1;
 };
 
-template <int BLOCK>
-__device__ __forceinline__ int vt_swizzle(int d) {
-  return ((d & 15) ^ ((d >> 4) & 7)) & (BLOCK / 8 - 1);
-}
+__device__ __forceinline__ int vt_slot(int d) { return d ^ ((d >> 4) & 7); }
 
 // Stored key-group (4 keys) kq holds the actual key group with bits 0 and 1 of its index swapped.
 __device__ __forceinline__ int actual_keygroup(int kq) {
   return (kq & ~3) | ((kq & 1) << 1) | ((kq >> 1) & 1);
 }
 
-// Staging registers for one K/V page on its way from global memory to LDS.
 template <int BLOCK, int HPW>
 struct Stage {
   u32x4_t k[TileCfg<BLOCK, HPW>::kKChunks];
   u32x4_t v[TileCfg<BLOCK, HPW>::kVGroups][4];
 };
 
-// K: 16-byte chunks, 16 consecutive threads per 256-byte row. V: every thread takes four
-// consecutive keys (one key group) at one 8-wide d slice so that it can write them transposed;
-// 16 consecutive threads still read whole rows.
+// Per-thread byte offsets of the page copy (fixed for the whole kernel).
 template <int BLOCK, int HPW>
-__device__ __forceinline__ void load_page(const uint16_t* __restrict__ kp,
-                                          const uint16_t* __restrict__ vp, int tid,
+struct CopyOffsets {
+  int k_glb, k_lds;              // K: chunk u adds u * (threads/16) rows
+  int v_glb[TileCfg<BLOCK, HPW>::kVGroups];
+  int v_lds[TileCfg<BLOCK, HPW>::kVGroups];
+  int v_xor;                     // row-slot XOR of this thread's 8 V^T rows
+};
+
+template <int BLOCK, int HPW>
+__device__ __forceinline__ CopyOffsets<BLOCK, HPW> copy_offsets(int tid) {
+  using Cfg = TileCfg<BLOCK, HPW>;
+  CopyOffsets<BLOCK, HPW> c;
+  c.k_glb = (tid >> 4) * (kHeadDim * 2) + (tid & 15) * 16;
+  c.k_lds = (tid >> 4) * Cfg::kKRow + (tid & 15) * 16;
+  const int dg = tid & 15;
+#pragma unroll
+  for (int u = 0; u < Cfg::kVGroups; ++u) {
+    const int kq = (u * Cfg::kThreads + tid) >> 4;
+    c.v_glb[u] = 4 * actual_keygroup(kq) * (kHeadDim * 2) + dg * 16;
+    c.v_lds[u] = 8 * dg * Cfg::kVRow + kq * 8;
+  }
+  c.v_xor = dg >> 1;
+  return c;
+}
+
+// Global -> registers for the page at byte offset `page` of this KV head (buffer loads: the page
+// offset is a scalar, per-thread offsets and chunk strides are fixed).
+template <int BLOCK, int HPW>
+__device__ __forceinline__ void load_page(__amdgpu_buffer_rsrc_t kr, __amdgpu_buffer_rsrc_t vr,
+                                          int page, const CopyOffsets<BLOCK, HPW>& c,
                                           Stage<BLOCK, HPW>& st) {
   using Cfg = TileCfg<BLOCK, HPW>;
 #pragma unroll
-  for (int u = 0; u < Cfg::kKChunks; ++u) {
-    const int id = u * Cfg::kThreads + tid;
-    st.k[u] = ldg16(kp + (id >> 4) * kHeadDim + (id & 15) * 8);
-  }
+  for (int u = 0; u < Cfg::kKChunks; ++u)
+    st.k[u] = __builtin_amdgcn_raw_buffer_load_b128(
+        kr, c.k_glb, page + u * (Cfg::kThreads / 16) * kHeadDim * 2, 0);
 #pragma unroll
-  for (int u = 0; u < Cfg::kVGroups; ++u) {
-    const int pi = u * Cfg::kThreads + tid;
-    const int kgi = actual_keygroup(pi >> 4), dg = pi & 15;
+  for (int u = 0; u < Cfg::kVGroups; ++u)
 #pragma unroll
-    for (int mm = 0; mm < 4; ++mm) st.v[u][mm] = ldg16(vp + (4 * kgi + mm) * kHeadDim + dg * 8);
-  }
+    for (int mm = 0; mm < 4; ++mm)
+      st.v[u][mm] = __builtin_amdgcn_raw_buffer_load_b128(vr, c.v_glb[u] + mm * kHeadDim * 2,
+                                                          page, 0);
 }
 
 template <int BLOCK, int HPW>
-__device__ __forceinline__ void store_k(uint16_t* Ks, const Stage<BLOCK, HPW>& st, int tid) {
+__device__ __forceinline__ void store_k(char* Kb, const Stage<BLOCK, HPW>& st,
+                                        const CopyOffsets<BLOCK, HPW>& c) {
   using Cfg = TileCfg<BLOCK, HPW>;
 #pragma unroll
-  for (int u = 0; u < Cfg::kKChunks; ++u) {
-    const int id = u * Cfg::kThreads + tid;
-    const int row = id >> 4, col = id & 15;
-    *reinterpret_cast<u32x4_t*>(Ks + row * kHeadDim + ((col ^ (row & 15)) << 3)) = st.k[u];
-  }
+  for (int u = 0; u < Cfg::kKChunks; ++u)
+    *reinterpret_cast<u32x4_t*>(Kb + c.k_lds + u * (Cfg::kThreads / 16) * Cfg::kKRow) = st.k[u];
 }
 
 template <int BLOCK, int HPW>
-__device__ __forceinline__ void store_vt(uint16_t* Vt, const Stage<BLOCK, HPW>& st, int tid) {
+__device__ __forceinline__ void store_vt(char* Vb, const Stage<BLOCK, HPW>& st,
+                                         const CopyOffsets<BLOCK, HPW>& c) {
   using Cfg = TileCfg<BLOCK, HPW>;
 #pragma unroll
   for (int u = 0; u < Cfg::kVGroups; ++u) {
-    const int pi = u * Cfg::kThreads + tid;
-    const int kq = pi >> 4, dg = pi & 15;
 #pragma unroll
     for (int e = 0; e < 8; ++e) {
-      const int d = 8 * dg + e;
       const int wd = e >> 1;
       const uint32_t k0 = st.v[u][0][wd], k1 = st.v[u][1][wd];
       const uint32_t k2 = st.v[u][2][wd], k3 = st.v[u][3][wd];
@@ -114,17 +139,13 @@ __device__ __forceinline__ void store_vt(uint16_t* Vt, const Stage<BLOCK, HPW>& 
         lo = (k0 & 0xffffu) | (k1 << 16);
         hi = (k2 & 0xffffu) | (k3 << 16);
       }
-      const int unit = kq ^ (2 * vt_swizzle<BLOCK>(d));
-      *reinterpret_cast<u32x2_t*>(Vt + d * BLOCK + unit * 4) = u32x2_t{lo, hi};
+      // row d = 8 dg + e lives at slot 8 dg + (e ^ (dg >> 1))
+      *reinterpret_cast<u32x2_t*>(Vb + c.v_lds[u] + (e ^ c.v_xor) * Cfg::kVRow) =
+          u32x2_t{lo, hi};
     }
   }
 }
 
-// Pipeline over the visited pages (one barrier per page, double-buffered LDS):
-//   prefetch page k+1 into registers | Q K^T of page k (and the tile's skip vote) |
-//   K of page k+1 -> LDS | barrier | skip decision, softmax, P V of page k | V of page k+1 -> LDS.
-// K buffer (k+1)%2 was last read by Q K^T of page k-1 and V buffer (k+1)%2 by P V of page k-1,
-// both finished by every wave before the barrier of page k.
 template <int BLOCK, int HPW, bool OSK>
 __global__ __attribute__((amdgpu_flat_work_group_size(TileCfg<BLOCK, HPW>::kThreads,
                                                       TileCfg<BLOCK, HPW>::kThreads)))
@@ -134,9 +155,11 @@ void attention_kernel(const AttnParams P) {
   using Cfg = TileCfg<BLOCK, HPW>;
   constexpr int KT = Cfg::kKeyTiles;
   constexpr int WPH = Cfg::kWavesPerHead;
-  __shared__ __attribute__((aligned(16))) uint16_t Ks[2][BLOCK * kHeadDim];
-  __shared__ __attribute__((aligned(16))) uint16_t Vt[2][kHeadDim * BLOCK];
+  constexpr int PAGE = BLOCK * kHeadDim * 2;  // bytes of one K or V page in global memory
+  __shared__ __attribute__((aligned(16))) char lds[Cfg::kLdsBytes];
   __shared__ float vote[2][Cfg::kWaves];
+  auto Kbuf = [&](int b) { return lds + b * Cfg::kKBytes; };
+  auto Vbuf = [&](int b) { return lds + 2 * Cfg::kKBytes + b * Cfg::kVBytes; };
 
   int unit, pair;
   if (!map_tile(blockIdx.x, P.G / HPW, P.n_units, unit, pair)) return;
@@ -151,6 +174,11 @@ void attention_kernel(const AttnParams P) {
   const size_t kv_off = (size_t)ng * P.L * kHeadDim;
   const size_t qo_off = (size_t)(n * P.Hq + h) * P.L * kHeadDim;
   const int qrow = i * BLOCK + wl * 32 + l32;
+  const __amdgpu_buffer_rsrc_t krs = __builtin_amdgcn_make_buffer_rsrc(
+      (void*)(P.a.k + kv_off), (short)0, P.L * kHeadDim * 2, 0x00020000);
+  const __amdgpu_buffer_rsrc_t vrs = __builtin_amdgcn_make_buffer_rsrc(
+      (void*)(P.a.v + kv_off), (short)0, P.L * kHeadDim * 2, 0x00020000);
+  const CopyOffsets<BLOCK, HPW> co = copy_offsets<BLOCK, HPW>(tid);
 
   // Q^T as the MFMA B operand: lane owns query row qrow, 8 chunks of 16 d (8 per lane half).
   bf16x8_t qf[8];
@@ -159,6 +187,13 @@ void attention_kernel(const AttnParams P) {
 #pragma unroll
     for (int c = 0; c < 8; ++c) qf[c] = as_bf16x8(ldg16(qp + 16 * c));
   }
+  // LDS read bases: K rows key = 32 t + l32 (t and the d chunk are immediates); V^T rows
+  // d = 32 dt + l32 through the row-slot swizzle (one base per dt, the key chunk is an immediate).
+  const int k_rd = l32 * Cfg::kKRow + half * 16;
+  int v_rd[4];
+#pragma unroll
+  for (int dt = 0; dt < 4; ++dt) v_rd[dt] = vt_slot(32 * dt + l32) * Cfg::kVRow + half * 16;
+
   // O^T accumulators: tile dt holds d = 32 dt + 8 (r / 4) + 4 half + r % 4 of row qrow.
   f32x16_t o[4];
 #pragma unroll
@@ -179,8 +214,6 @@ void attention_kernel(const AttnParams P) {
   }
   const size_t log_off = ((size_t)(n * P.Hq + h) * P.nb + i) * P.nb;
   int ncomp = 0;
-  const uint16_t* kbase = P.a.k + kv_off;
-  const uint16_t* vbase = P.a.v + kv_off;
 
   // A malformed list entry (outside [0, i]) is visited as block i but contributes nothing.
   auto entry = [&](int kk, bool& valid) -> int {
@@ -199,10 +232,9 @@ void attention_kernel(const AttnParams P) {
   int j_cur = 0;
   if (cnt > 0) {
     j_cur = entry(0, v_cur);
-    load_page<BLOCK, HPW>(kbase + (size_t)j_cur * BLOCK * kHeadDim,
-                          vbase + (size_t)j_cur * BLOCK * kHeadDim, tid, st);
-    store_k<BLOCK, HPW>(Ks[0], st, tid);
-    store_vt<BLOCK, HPW>(Vt[0], st, tid);
+    load_page<BLOCK, HPW>(krs, vrs, j_cur * PAGE, co, st);
+    store_k<BLOCK, HPW>(Kbuf(0), st, co);
+    store_vt<BLOCK, HPW>(Vbuf(0), st, co);
   }
   __syncthreads();
 
@@ -211,36 +243,26 @@ void attention_kernel(const AttnParams P) {
     const bool has_next = kk + 1 < cnt;
     bool v_next = false;
     int j_next = 0;
-    int tx = tid;  // per-thread copy offsets, recomputed each page (see lx below)
-    asm volatile("" : "+v"(tx));
     if (has_next) {
       j_next = entry(kk + 1, v_next);
-      load_page<BLOCK, HPW>(kbase + (size_t)j_next * BLOCK * kHeadDim,
-                            vbase + (size_t)j_next * BLOCK * kHeadDim, tx, st);
+      load_page<BLOCK, HPW>(krs, vrs, j_next * PAGE, co, st);
     }
 
-    // The swizzled LDS offsets are cheap to recompute; keeping them out of loop-invariant code
-    // motion saves ~40 registers that would otherwise stay live across the whole page loop.
-    int lx = l32;
-    asm volatile("" : "+v"(lx));
     // S^T tile t: keys 32 t + 8 (r / 4) + 4 half + r % 4 (register r) of query row qrow.
     f32x16_t s[KT];
-    float mnew = m;
-    const uint16_t* Kb = Ks[buf];
+    const char* Kb = Kbuf(buf) + k_rd;
 #pragma unroll
     for (int t = 0; t < KT; ++t) {
-      const int key = 32 * t + lx;
       f32x16_t acc;
 #pragma unroll
       for (int r = 0; r < 16; ++r) acc[r] = 0.f;
 #pragma unroll
       for (int c = 0; c < 8; ++c) {
-        const bf16x8_t kf = as_bf16x8(*reinterpret_cast<const u32x4_t*>(
-            Kb + key * kHeadDim + (((2 * c + half) ^ (lx & 15)) << 3)));
+        const bf16x8_t kf = as_bf16x8(
+            *reinterpret_cast<const u32x4_t*>(Kb + t * 32 * Cfg::kKRow + c * 32));
         acc = mfma32x32x16(kf, qf[c], acc);
       }
       s[t] = acc;
-      __builtin_amdgcn_sched_barrier(0);  // bound the live fragments to one key tile
     }
     if (j_cur == i) {  // diagonal block: causal mask inside the tile
       const int qi = wl * 32 + l32;
@@ -258,13 +280,13 @@ void attention_kernel(const AttnParams P) {
 #pragma unroll
       for (int r = 0; r < 16; ++r) mloc = fmaxf(mloc, s[t][r]);
     mloc = fmaxf(mloc, swap_halves(mloc));
-    if (v_cur) mnew = fmaxf(m, mloc);
+    const float mnew = v_cur ? fmaxf(m, mloc) : m;
     if constexpr (OSK) {
       // Eq. (skip): each head's b-row tile votes with its largest (m_loc - m), in nats.
       const float marg = wave_max((mloc - mnew) * P.scale);
       if (lane == 0) vote[buf][w] = marg;
     }
-    if (has_next) store_k<BLOCK, HPW>(Ks[buf ^ 1], st, tx);
+    if (has_next) store_k<BLOCK, HPW>(Kbuf(buf ^ 1), st, co);
     __syncthreads();
 
     bool skip = !v_cur;
@@ -295,12 +317,14 @@ void attention_kernel(const AttnParams P) {
           rs += pv;
         }
       lsum = fmaf(lsum, alpha, rs);
+      if (__any(alpha != 1.f)) {  // the running max moved in some row of this wave
 #pragma unroll
-      for (int dt = 0; dt < 4; ++dt)
+        for (int dt = 0; dt < 4; ++dt)
 #pragma unroll
-        for (int r = 0; r < 16; ++r) o[dt][r] *= alpha;
+          for (int r = 0; r < 16; ++r) o[dt][r] *= alpha;
+      }
       // O^T += V^T P^T over 16-key chunks kc; P^T chunk kc = registers 8 (kc % 2) .. +7 of tile kc / 2.
-      const uint16_t* Vb = Vt[buf];
+      const char* Vb = Vbuf(buf);
 #pragma unroll
       for (int kc = 0; kc < BLOCK / 16; ++kc) {
         bf16x8_t pf;
@@ -308,21 +332,14 @@ void attention_kernel(const AttnParams P) {
         for (int e = 0; e < 8; ++e) pf[e] = (__bf16)s[kc >> 1][8 * (kc & 1) + e];
 #pragma unroll
         for (int dt = 0; dt < 4; ++dt) {
-          const int d = 32 * dt + lx;
-          const int u = (4 * kc + 2 * half) ^ (2 * vt_swizzle<BLOCK>(d));
           const bf16x8_t vf =
-              as_bf16x8(*reinterpret_cast<const u32x4_t*>(Vb + d * BLOCK + u * 4));
+              as_bf16x8(*reinterpret_cast<const u32x4_t*>(Vb + v_rd[dt] + kc * 32));
           o[dt] = mfma32x32x16(vf, pf, o[dt]);
         }
-        if (kc & 1) __builtin_amdgcn_sched_barrier(0);  // and to two 16-key chunks of V
       }
       ++ncomp;
     }
-    if (has_next) {
-      int ty = tid;
-      asm volatile("" : "+v"(ty));
-      store_vt<BLOCK, HPW>(Vt[buf ^ 1], st, ty);
-    }
+    if (has_next) store_vt<BLOCK, HPW>(Vbuf(buf ^ 1), st, co);
     j_cur = j_next;
     v_cur = v_next;
   }
