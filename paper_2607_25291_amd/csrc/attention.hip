@@ -2,33 +2,39 @@
 //
 // A workgroup computes HPW query heads of one KV group for one query block of b rows: b/32
 // wavefronts per head, 32 query rows per wavefront. The K and V pages of each visited key block are
-// staged through LDS once and serve every head of the workgroup. Logits are formed transposed,
+// fetched once into LDS and serve every head of the workgroup. Logits are formed transposed,
 // S^T = K Q^T, with bf16 MFMA 32x32x16 so that every lane owns one query row; the online softmax
 // runs in fp32 (Sec. 3.1). OSK walks the KAP list (Algorithm A, attention loop) and after Q K^T
 // decides, for each head's whole b-row tile at once, whether the value side can be skipped
 // (Eq. (skip)); the dense kernel visits j = 0..i in order and never skips.
 //
-// Pipeline (double-buffered LDS, one barrier per page): the next page's global loads are issued
-// into registers, Q K^T of the current page runs (and each wave posts its skip-vote value), the
-// next K page goes to LDS, barrier, the tile decides, softmax and P V run, the next V page goes to
-// LDS. K buffer (k+1)%2 was last read by Q K^T of page k-1 and V buffer (k+1)%2 by P V of page k-1,
-// both finished by every wave before the barrier of page k.
+// Pages move from HBM straight into LDS (buffer loads with an LDS destination: no registers are
+// spent on staging), double-buffered, with one barrier per page m:
+//   Q K^T of page m, each wave posts its skip-vote value | wait for this wave's loads | barrier |
+//   issue V of page m+1 and K of page m+2 | skip decision, softmax, P V of page m.
+// K buffer m%2 is refilled right after the barrier that follows the last Q K^T on it, V buffer
+// (m+1)%2 right after the barrier that follows the last P V on it; each load has a whole page of
+// work to land before the barrier that publishes it.
 //
-// LDS layouts (64 banks x 4 bytes; rows padded by 16 bytes so that 16 consecutive rows start in 16
-// different 4-bank groups):
-//   K  [key][d]  row-major, 272-byte rows. MFMA A-operand reads (lane = key, 16 bytes of d) and the
-//                coalesced row writes are conflict-free; read addresses are one base register plus
-//                immediates.
-//   Vt [d][key'] V transposed, so that the P V MFMA reads eight keys of one d as 16 bytes. Keys are
-//                permuted inside every 16 (offset bits 2 and 3 swapped) so that those eight keys are
-//                the eight the lane holds in P^T. Row d is stored at row slot d ^ ((d / 16) % 8), which
-//                keeps both the 16-byte reads (16 consecutive d) and the transposing 8-byte writes
-//                (d = 8 g + e for 16 values of g) conflict-free.
+// LDS layouts (one 16-byte slot of 8 values at a time; a direct load writes 64 consecutive slots,
+// each lane picks the global slot that belongs there):
+//   K [key][d]  256-byte rows, slot s of row r stored at slot s ^ (r % 16). The MFMA A-operand reads
+//               (lane = key, 16 bytes of d) of 16 consecutive keys hit 16 different slots.
+//   V [key][d]  256-byte rows, slot s of row r stored at slot s ^ 4 (r % 4). P V takes V through
+//               transposing LDS reads (ds_read_b64_tr_b16): in each 16-lane group the lane i receives,
+//               for k = 0..3, element i % 4 of the 8 bytes addressed by lane 4k + i / 4. Lane i
+//               addressing V[key0 + i/4][d0 + 4 (i%4)] therefore receives keys key0..key0+3 of
+//               column d0 + i, which is the P^T key set that lane holds from the S^T accumulators.
+#include <type_traits>
+
 #include "cosa_device.h"
 #include "cosa_internal.h"
 
 namespace cosa {
 namespace {
+
+typedef short s16x4_t __attribute__((ext_vector_type(4)));
+#define COSA_LDS(p) ((__attribute__((address_space(3))) void*)(p))
 
 struct AttnParams {
   AttnArgs a;
@@ -42,107 +48,31 @@ struct TileCfg {
   static constexpr int kWaves = HPW * kWavesPerHead;
   static constexpr int kThreads = kWaves * 64;
   static constexpr int kKeyTiles = BLOCK / 32;
-  static constexpr int kKChunks = BLOCK * 16 / kThreads;  // 16-byte K chunks per thread
-  static constexpr int kVGroups = BLOCK * 4 / kThreads;   // (4-key group, 8-wide d slice) per thread
-  static constexpr int kKRow = (kHeadDim + 8) * 2;        // bytes per K row in LDS
-  static constexpr int kVRow = (BLOCK + 8) * 2;           // bytes per V^T row in LDS
-  static constexpr int kKBytes = BLOCK * kKRow;
-  static constexpr int kVBytes = kHeadDim * kVRow;
-  static constexpr int kLdsBytes = 2 * (kKBytes + kVBytes);
+  static constexpr int kPage = BLOCK * kHeadDim * 2;         // bytes of one K or V page
+  static constexpr int kChunks = kPage / 1024;               // 1 KiB direct-load chunks per page
+  static constexpr int kChunksPerWave = kChunks / kWaves;
+  static constexpr int kLdsBytes = 4 * kPage;
   static constexpr int kWgPerCu = (160 * 1024) / (kLdsBytes + 256);
   static constexpr int kWavesPerEu = (kWgPerCu * kWaves) / 4 > 1 ? (kWgPerCu * kWaves) / 4 : 1;
+  static_assert(kChunks % kWaves == 0, "page chunks must split evenly over the waves");
 };
 
-__device__ __forceinline__ int vt_slot(int d) { return d ^ ((d >> 4) & 7); }
-
-// Stored key-group (4 keys) kq holds the actual key group with bits 0 and 1 of its index swapped.
-__device__ __forceinline__ int actual_keygroup(int kq) {
-  return (kq & ~3) | ((kq & 1) << 1) | ((kq >> 1) & 1);
-}
-
-template <int BLOCK, int HPW>
-struct Stage {
-  u32x4_t k[TileCfg<BLOCK, HPW>::kKChunks];
-  u32x4_t v[TileCfg<BLOCK, HPW>::kVGroups][4];
-};
-
-// Per-thread byte offsets of the page copy (fixed for the whole kernel).
-template <int BLOCK, int HPW>
-struct CopyOffsets {
-  int k_glb, k_lds;              // K: chunk u adds u * (threads/16) rows
-  int v_glb[TileCfg<BLOCK, HPW>::kVGroups];
-  int v_lds[TileCfg<BLOCK, HPW>::kVGroups];
-  int v_xor;                     // row-slot XOR of this thread's 8 V^T rows
-};
-
-template <int BLOCK, int HPW>
-__device__ __forceinline__ CopyOffsets<BLOCK, HPW> copy_offsets(int tid) {
-  using Cfg = TileCfg<BLOCK, HPW>;
-  CopyOffsets<BLOCK, HPW> c;
-  c.k_glb = (tid >> 4) * (kHeadDim * 2) + (tid & 15) * 16;
-  c.k_lds = (tid >> 4) * Cfg::kKRow + (tid & 15) * 16;
-  const int dg = tid & 15;
-#pragma unroll
-  for (int u = 0; u < Cfg::kVGroups; ++u) {
-    const int kq = (u * Cfg::kThreads + tid) >> 4;
-    c.v_glb[u] = 4 * actual_keygroup(kq) * (kHeadDim * 2) + dg * 16;
-    c.v_lds[u] = 8 * dg * Cfg::kVRow + kq * 8;
-  }
-  c.v_xor = dg >> 1;
-  return c;
-}
-
-// Global -> registers for the page at byte offset `page` of this KV head (buffer loads: the page
-// offset is a scalar, per-thread offsets and chunk strides are fixed).
-template <int BLOCK, int HPW>
-__device__ __forceinline__ void load_page(__amdgpu_buffer_rsrc_t kr, __amdgpu_buffer_rsrc_t vr,
-                                          int page, const CopyOffsets<BLOCK, HPW>& c,
-                                          Stage<BLOCK, HPW>& st) {
+// Direct global -> LDS copy of one page: wave w moves chunks c = u * waves + w (rows 4c .. 4c+3).
+// Lane l fills LDS slot l of the chunk (row 4c + l/16, stored slot l%16) with the global slot that
+// the layout puts there. The page offset and the chunk offset are scalars.
+template <int BLOCK, int HPW, bool IS_K>
+__device__ __forceinline__ void copy_page(__amdgpu_buffer_rsrc_t rs, char* dst, int page_off,
+                                          int w, int lane) {
   using Cfg = TileCfg<BLOCK, HPW>;
 #pragma unroll
-  for (int u = 0; u < Cfg::kKChunks; ++u)
-    st.k[u] = __builtin_amdgcn_raw_buffer_load_b128(
-        kr, c.k_glb, page + u * (Cfg::kThreads / 16) * kHeadDim * 2, 0);
-#pragma unroll
-  for (int u = 0; u < Cfg::kVGroups; ++u)
-#pragma unroll
-    for (int mm = 0; mm < 4; ++mm)
-      st.v[u][mm] = __builtin_amdgcn_raw_buffer_load_b128(vr, c.v_glb[u] + mm * kHeadDim * 2,
-                                                          page, 0);
-}
-
-template <int BLOCK, int HPW>
-__device__ __forceinline__ void store_k(char* Kb, const Stage<BLOCK, HPW>& st,
-                                        const CopyOffsets<BLOCK, HPW>& c) {
-  using Cfg = TileCfg<BLOCK, HPW>;
-#pragma unroll
-  for (int u = 0; u < Cfg::kKChunks; ++u)
-    *reinterpret_cast<u32x4_t*>(Kb + c.k_lds + u * (Cfg::kThreads / 16) * Cfg::kKRow) = st.k[u];
-}
-
-template <int BLOCK, int HPW>
-__device__ __forceinline__ void store_vt(char* Vb, const Stage<BLOCK, HPW>& st,
-                                         const CopyOffsets<BLOCK, HPW>& c) {
-  using Cfg = TileCfg<BLOCK, HPW>;
-#pragma unroll
-  for (int u = 0; u < Cfg::kVGroups; ++u) {
-#pragma unroll
-    for (int e = 0; e < 8; ++e) {
-      const int wd = e >> 1;
-      const uint32_t k0 = st.v[u][0][wd], k1 = st.v[u][1][wd];
-      const uint32_t k2 = st.v[u][2][wd], k3 = st.v[u][3][wd];
-      uint32_t lo, hi;
-      if (e & 1) {
-        lo = (k0 >> 16) | (k1 & 0xffff0000u);
-        hi = (k2 >> 16) | (k3 & 0xffff0000u);
-      } else {
-        lo = (k0 & 0xffffu) | (k1 << 16);
-        hi = (k2 & 0xffffu) | (k3 << 16);
-      }
-      // row d = 8 dg + e lives at slot 8 dg + (e ^ (dg >> 1))
-      *reinterpret_cast<u32x2_t*>(Vb + c.v_lds[u] + (e ^ c.v_xor) * Cfg::kVRow) =
-          u32x2_t{lo, hi};
-    }
+  for (int u = 0; u < Cfg::kChunksPerWave; ++u) {
+    const int c = u * Cfg::kWaves + w;
+    const int row = 4 * c + (lane >> 4);
+    const int stored = lane & 15;
+    const int slot = IS_K ? (stored ^ (row & 15)) : (stored ^ ((row & 3) << 2));
+    const int voff = (lane >> 4) * (kHeadDim * 2) + slot * 16;
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, COSA_LDS(dst + c * 1024), 16, voff,
+                                             page_off + c * 1024, 0, 0);
   }
 }
 
@@ -155,11 +85,14 @@ void attention_kernel(const AttnParams P) {
   using Cfg = TileCfg<BLOCK, HPW>;
   constexpr int KT = Cfg::kKeyTiles;
   constexpr int WPH = Cfg::kWavesPerHead;
-  constexpr int PAGE = BLOCK * kHeadDim * 2;  // bytes of one K or V page in global memory
-  __shared__ __attribute__((aligned(16))) char lds[Cfg::kLdsBytes];
+  constexpr int PAGE = Cfg::kPage;
+  // V buffers first: they get the low 64 KiB, where every transposing read's buffer and key offsets
+  // fit the instruction's immediate (the K reads add their buffer base once per d chunk).
+  __shared__ __attribute__((aligned(1024))) char v_lds0[PAGE];
+  __shared__ __attribute__((aligned(1024))) char v_lds1[PAGE];
+  __shared__ __attribute__((aligned(1024))) char k_lds0[PAGE];
+  __shared__ __attribute__((aligned(1024))) char k_lds1[PAGE];
   __shared__ float vote[2][Cfg::kWaves];
-  auto Kbuf = [&](int b) { return lds + b * Cfg::kKBytes; };
-  auto Vbuf = [&](int b) { return lds + 2 * Cfg::kKBytes + b * Cfg::kVBytes; };
 
   int unit, pair;
   if (!map_tile(blockIdx.x, P.G / HPW, P.n_units, unit, pair)) return;
@@ -178,30 +111,6 @@ void attention_kernel(const AttnParams P) {
       (void*)(P.a.k + kv_off), (short)0, P.L * kHeadDim * 2, 0x00020000);
   const __amdgpu_buffer_rsrc_t vrs = __builtin_amdgcn_make_buffer_rsrc(
       (void*)(P.a.v + kv_off), (short)0, P.L * kHeadDim * 2, 0x00020000);
-  const CopyOffsets<BLOCK, HPW> co = copy_offsets<BLOCK, HPW>(tid);
-
-  // Q^T as the MFMA B operand: lane owns query row qrow, 8 chunks of 16 d (8 per lane half).
-  bf16x8_t qf[8];
-  {
-    const uint16_t* qp = P.a.q + qo_off + (size_t)qrow * kHeadDim + 8 * half;
-#pragma unroll
-    for (int c = 0; c < 8; ++c) qf[c] = as_bf16x8(ldg16(qp + 16 * c));
-  }
-  // LDS read bases: K rows key = 32 t + l32 (t and the d chunk are immediates); V^T rows
-  // d = 32 dt + l32 through the row-slot swizzle (one base per dt, the key chunk is an immediate).
-  const int k_rd = l32 * Cfg::kKRow + half * 16;
-  int v_rd[4];
-#pragma unroll
-  for (int dt = 0; dt < 4; ++dt) v_rd[dt] = vt_slot(32 * dt + l32) * Cfg::kVRow + half * 16;
-
-  // O^T accumulators: tile dt holds d = 32 dt + 8 (r / 4) + 4 half + r % 4 of row qrow.
-  f32x16_t o[4];
-#pragma unroll
-  for (int dt = 0; dt < 4; ++dt)
-#pragma unroll
-    for (int r = 0; r < 16; ++r) o[dt][r] = 0.f;
-  float m = -INFINITY;  // running row max (raw logits), identical in both lane halves
-  float lsum = 0.f;     // this lane half's partial row sum
 
   int cnt;
   const int32_t* lst = nullptr;
@@ -212,67 +121,101 @@ void attention_kernel(const AttnParams P) {
   } else {
     cnt = i + 1;
   }
+  // List entries, read ahead of their use. A malformed entry (outside [0, i]) is fetched as block
+  // i but contributes nothing.
+  auto raw_entry = [&](int kk) -> int {
+    if constexpr (OSK) return kk < cnt ? lst[kk] : 0;
+    else return kk;
+  };
+  auto page_of = [&](int raw) -> int { return (unsigned)raw <= (unsigned)i ? raw : i; };
+
+  // Prologue: K and V of page 0, K of page 1.
+  int raw0 = __builtin_amdgcn_readfirstlane(raw_entry(0));
+  int raw1 = __builtin_amdgcn_readfirstlane(raw_entry(1));
+  int raw2 = raw_entry(2);  // becomes scalar after the first barrier
+  if (cnt > 0) {
+    copy_page<BLOCK, HPW, true>(krs, k_lds0, page_of(raw0) * PAGE, w, lane);
+    copy_page<BLOCK, HPW, false>(vrs, v_lds0, page_of(raw0) * PAGE, w, lane);
+  }
+  if (cnt > 1) copy_page<BLOCK, HPW, true>(krs, k_lds1, page_of(raw1) * PAGE, w, lane);
+
+  // Q^T as the MFMA B operand: lane owns query row qrow, 8 chunks of 16 d (8 per lane half).
+  bf16x8_t qf[8];
+  {
+    const uint16_t* qp = P.a.q + qo_off + (size_t)qrow * kHeadDim + 8 * half;
+#pragma unroll
+    for (int c = 0; c < 8; ++c) qf[c] = as_bf16x8(ldg16(qp + 16 * c));
+  }
+  // O^T accumulators: tile dt holds d = 32 dt + 8 (r / 4) + 4 half + r % 4 of row qrow.
+  f32x16_t o[4];
+#pragma unroll
+  for (int dt = 0; dt < 4; ++dt)
+#pragma unroll
+    for (int r = 0; r < 16; ++r) o[dt][r] = 0.f;
+  float m = -INFINITY;  // running row max (raw logits), identical in both lane halves
+  float lsum = 0.f;     // this lane half's partial row sum
+
+  // LDS read offsets. K: key 32 t + l32, d slot 2 c + half (t is an immediate). V: transposing
+  // reads of rows 32 t + 16 c2 + 8 a + 4 half + (i / 4) and d = 32 dt + 16 g16 + 4 (i % 4), with
+  // i = lane % 16 and g16 = (lane / 16) % 2 (t, c2, a are immediates; one offset per dt).
+  int k_rd[8];
+#pragma unroll
+  for (int c = 0; c < 8; ++c) k_rd[c] = l32 * 256 + (((2 * c + half) ^ (l32 & 15)) << 4);
+  int v_rd[4];
+  {
+    const int li = lane & 15, g16 = (lane >> 4) & 1;
+#pragma unroll
+    for (int dt = 0; dt < 4; ++dt) {
+      const int slot = 4 * dt + 2 * g16 + ((li & 3) >> 1);
+      v_rd[dt] = (4 * half + (li >> 2)) * 256 + ((slot ^ ((li >> 2) << 2)) << 4) + 8 * (li & 1);
+    }
+  }
   const size_t log_off = ((size_t)(n * P.Hq + h) * P.nb + i) * P.nb;
   int ncomp = 0;
+  int j_cur = page_of(raw0);
+  bool v_cur = OSK ? ((unsigned)raw0 <= (unsigned)i) : true;
+  int raw_a = raw1;  // entry m+1 (scalar)
 
-  // A malformed list entry (outside [0, i]) is visited as block i but contributes nothing.
-  auto entry = [&](int kk, bool& valid) -> int {
-    if constexpr (OSK) {
-      const int j = lst[kk];
-      valid = (unsigned)j <= (unsigned)i;
-      return valid ? j : i;
-    } else {
-      valid = true;
-      return kk;
-    }
-  };
-
-  Stage<BLOCK, HPW> st;
-  bool v_cur = false;
-  int j_cur = 0;
-  if (cnt > 0) {
-    j_cur = entry(0, v_cur);
-    load_page<BLOCK, HPW>(krs, vrs, j_cur * PAGE, co, st);
-    store_k<BLOCK, HPW>(Kbuf(0), st, co);
-    store_vt<BLOCK, HPW>(Vbuf(0), st, co);
-  }
+  __builtin_amdgcn_s_waitcnt(0);  // prologue pages and Q fragments
   __syncthreads();
 
-  for (int kk = 0; kk < cnt; ++kk) {
-    const int buf = kk & 1;
-    const bool has_next = kk + 1 < cnt;
-    bool v_next = false;
-    int j_next = 0;
-    if (has_next) {
-      j_next = entry(kk + 1, v_next);
-      load_page<BLOCK, HPW>(krs, vrs, j_next * PAGE, co, st);
-    }
+  // One page of the walk. BUF selects the LDS buffers at compile time, so that every LDS access
+  // names one fixed array: reads of this page's buffers never wait for the in-flight copies into
+  // the other ones, and buffer offsets fold into instruction immediates.
+  auto step = [&](int kk, auto bufc) {
+    constexpr int BUF = decltype(bufc)::value;
+    const char* Kb = BUF ? k_lds1 : k_lds0;
+    const char* Vb = BUF ? v_lds1 : v_lds0;
 
-    // S^T tile t: keys 32 t + 8 (r / 4) + 4 half + r % 4 (register r) of query row qrow.
+    // S^T tile t: keys 32 t + 8 (r / 4) + 4 half + r % 4 (register r) of query row qrow. The d chunk
+    // is the outer loop: the KT tiles are independent accumulation chains, and each chunk's KT
+    // fragments are read from LDS as one batch.
     f32x16_t s[KT];
-    const char* Kb = Kbuf(buf) + k_rd;
 #pragma unroll
-    for (int t = 0; t < KT; ++t) {
-      f32x16_t acc;
+    for (int t = 0; t < KT; ++t)
 #pragma unroll
-      for (int r = 0; r < 16; ++r) acc[r] = 0.f;
+      for (int r = 0; r < 16; ++r) s[t][r] = 0.f;
 #pragma unroll
-      for (int c = 0; c < 8; ++c) {
-        const bf16x8_t kf = as_bf16x8(
-            *reinterpret_cast<const u32x4_t*>(Kb + t * 32 * Cfg::kKRow + c * 32));
-        acc = mfma32x32x16(kf, qf[c], acc);
-      }
-      s[t] = acc;
+    for (int c = 0; c < 8; ++c) {
+      bf16x8_t kf[KT];
+#pragma unroll
+      for (int t = 0; t < KT; ++t)
+        kf[t] = as_bf16x8(*reinterpret_cast<const u32x4_t*>(Kb + k_rd[c] + t * 32 * 256));
+#pragma unroll
+      for (int t = 0; t < KT; ++t) s[t] = mfma32x32x16(kf[t], qf[c], s[t]);
+      __builtin_amdgcn_sched_group_barrier(0x100, KT, 0);  // the chunk's LDS reads ...
+      __builtin_amdgcn_sched_group_barrier(0x008, KT, 0);  // ... then its MFMAs
     }
     if (j_cur == i) {  // diagonal block: causal mask inside the tile
-      const int qi = wl * 32 + l32;
+      // key 32 t + 8 (r / 4) + 4 half + r % 4 > query wl*32 + l32, with the lane part moved to the
+      // right-hand side so that every compare is against an immediate
+      int qh = wl * 32 + l32 - 4 * half;
+      asm volatile("" : "+v"(qh));
 #pragma unroll
       for (int t = 0; t < KT; ++t)
 #pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          const int key = 32 * t + 8 * (r >> 2) + 4 * half + (r & 3);
-          if (key > qi) s[t][r] = -INFINITY;
-        }
+        for (int r = 0; r < 16; ++r)
+          if (32 * t + 8 * (r >> 2) + (r & 3) > qh) s[t][r] = -INFINITY;
     }
     float mloc = -INFINITY;
 #pragma unroll
@@ -284,17 +227,25 @@ void attention_kernel(const AttnParams P) {
     if constexpr (OSK) {
       // Eq. (skip): each head's b-row tile votes with its largest (m_loc - m), in nats.
       const float marg = wave_max((mloc - mnew) * P.scale);
-      if (lane == 0) vote[buf][w] = marg;
+      if (lane == 0) vote[BUF][w] = marg;
     }
-    if (has_next) store_k<BLOCK, HPW>(Kbuf(buf ^ 1), st, co);
+    __builtin_amdgcn_s_waitcnt(0);  // V of page m and K of page m+1 have landed (this wave's part)
     __syncthreads();
+
+    // Pages m+1 (V) and m+2 (K) can now be overwritten by their successors.
+    const int raw_b = __builtin_amdgcn_readfirstlane(raw2);  // entry m+2
+    raw2 = raw_entry(kk + 3);
+    if (kk + 1 < cnt)
+      copy_page<BLOCK, HPW, false>(vrs, BUF ? v_lds0 : v_lds1, page_of(raw_a) * PAGE, w, lane);
+    if (kk + 2 < cnt)
+      copy_page<BLOCK, HPW, true>(krs, BUF ? k_lds1 : k_lds0, page_of(raw_b) * PAGE, w, lane);
 
     bool skip = !v_cur;
     if constexpr (OSK) {
       if (v_cur) {
-        float dk = vote[buf][hw * WPH];
+        float dk = vote[BUF][hw * WPH];
 #pragma unroll
-        for (int ww = 1; ww < WPH; ++ww) dk = fmaxf(dk, vote[buf][hw * WPH + ww]);
+        for (int ww = 1; ww < WPH; ++ww) dk = fmaxf(dk, vote[BUF][hw * WPH + ww]);
         skip = P.a.skip_on && (dk < P.a.tau);
         if (wl == 0 && lane == 0) {
           if (P.a.visit_log) P.a.visit_log[log_off + kk] = skip ? 2 : 1;
@@ -323,25 +274,40 @@ void attention_kernel(const AttnParams P) {
 #pragma unroll
           for (int r = 0; r < 16; ++r) o[dt][r] *= alpha;
       }
-      // O^T += V^T P^T over 16-key chunks kc; P^T chunk kc = registers 8 (kc % 2) .. +7 of tile kc / 2.
-      const char* Vb = Vbuf(buf);
+      // O^T += V^T P^T over 16-key chunks kc = 2 t + c2: P^T element e of the chunk is register
+      // 8 c2 + e of tile t (key 32 t + 16 c2 + 8 (e / 4) + 4 half + e % 4); the V^T operand is the
+      // matching pair of transposing reads (e / 4 = a).
 #pragma unroll
       for (int kc = 0; kc < BLOCK / 16; ++kc) {
         bf16x8_t pf;
 #pragma unroll
         for (int e = 0; e < 8; ++e) pf[e] = (__bf16)s[kc >> 1][8 * (kc & 1) + e];
+        bf16x8_t vf[4];
 #pragma unroll
         for (int dt = 0; dt < 4; ++dt) {
-          const bf16x8_t vf =
-              as_bf16x8(*reinterpret_cast<const u32x4_t*>(Vb + v_rd[dt] + kc * 32));
-          o[dt] = mfma32x32x16(vf, pf, o[dt]);
+          const char* vp = Vb + v_rd[dt] + kc * 16 * 256;
+          const s16x4_t lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+              (__attribute__((address_space(3))) s16x4_t*)(vp));
+          const s16x4_t hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+              (__attribute__((address_space(3))) s16x4_t*)(vp + 8 * 256));
+          vf[dt] = __builtin_bit_cast(bf16x8_t,
+                                      __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
         }
+#pragma unroll
+        for (int dt = 0; dt < 4; ++dt) o[dt] = mfma32x32x16(vf[dt], pf, o[dt]);
+        __builtin_amdgcn_sched_group_barrier(0x100, 8, 0);  // the chunk's transposing reads ...
+        __builtin_amdgcn_sched_group_barrier(0x008, 4, 0);  // ... then its MFMAs
       }
       ++ncomp;
     }
-    if (has_next) store_vt<BLOCK, HPW>(Vbuf(buf ^ 1), st, co);
-    j_cur = j_next;
-    v_cur = v_next;
+    j_cur = page_of(raw_a);
+    v_cur = OSK ? ((unsigned)raw_a <= (unsigned)i) : true;
+    raw_a = raw_b;
+  };
+
+  for (int kk = 0; kk < cnt; kk += 2) {
+    step(kk, std::integral_constant<int, 0>{});
+    if (kk + 1 < cnt) step(kk + 1, std::integral_constant<int, 1>{});
   }
 
   lsum += swap_halves(lsum);
