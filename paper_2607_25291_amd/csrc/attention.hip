@@ -9,13 +9,16 @@
 // (Eq. (skip)); the dense kernel visits j = 0..i in order and never skips.
 //
 // Pages move from HBM straight into LDS (buffer loads with an LDS destination: no registers are
-// spent on staging), double-buffered, with one barrier per page m:
-//   Q K^T of page m, each wave posts its skip-vote value | wait for this wave's loads | barrier |
-//   issue V of page m+1 and K of page m+2 | skip decision, softmax, P V of page m.
-// K buffer m%2 is refilled right after the barrier that follows the last Q K^T on it, V buffer
-// (m+1)%2 right after the barrier that follows the last P V on it; each load has a whole page of
-// work to land before the barrier that publishes it.
-//
+// spent on staging), double-buffered. Each wave works through its pages in two halves,
+//   QK(m): Q K^T of page m, the diagonal mask, the new running max and the wave's skip vote;
+//   PV(m): the skip decision from the votes, softmax, P V of page m;
+// with a workgroup barrier after each half. With two heads in a workgroup the waves of the second
+// head start one barrier later, so phase 2m runs QK(m) of head 0 beside PV(m-1) of head 1 and phase
+// 2m+1 runs PV(m) of head 0 beside QK(m) of head 1. Waves w and w + 4 share a SIMD: while one
+// issues the Q K^T MFMAs the other runs its softmax VALU work and P V MFMAs. The waves of head 0
+// fetch K pages (page m+1 at the start of QK(m)), those of head 1 V pages (page m+1 at the start of
+// their QK(m)); a single head fetches both. A wave waits for its own copies at the end of its PV
+// half, so every copy has two phases to land before the barrier that publishes it.
 // LDS layouts (one 16-byte slot of 8 values at a time; a direct load writes 64 consecutive slots,
 // each lane picks the global slot that belongs there):
 //   K [key][d]  256-byte rows, slot s of row r stored at slot s ^ (r % 16). The MFMA A-operand reads
@@ -36,6 +39,11 @@ namespace {
 typedef short s16x4_t __attribute__((ext_vector_type(4)));
 #define COSA_LDS(p) ((__attribute__((address_space(3))) void*)(p))
 
+// s_waitcnt immediates (vmcnt in bits 3:0 and 15:14, expcnt 6:4, lgkmcnt 11:8): wait for vector
+// memory and LDS operations, or for LDS operations only.
+constexpr int kVmcntLgkm0 = 0x0070;
+constexpr int kLgkm0 = 0xC07F;
+
 struct AttnParams {
   AttnArgs a;
   int Hq, Hkv, L, nb, G, n_units;
@@ -49,30 +57,34 @@ struct TileCfg {
   static constexpr int kThreads = kWaves * 64;
   static constexpr int kKeyTiles = BLOCK / 32;
   static constexpr int kPage = BLOCK * kHeadDim * 2;         // bytes of one K or V page
-  static constexpr int kChunks = kPage / 1024;               // 1 KiB direct-load chunks per page
-  static constexpr int kChunksPerWave = kChunks / kWaves;
   static constexpr int kLdsBytes = 4 * kPage;
   static constexpr int kWgPerCu = (160 * 1024) / (kLdsBytes + 256);
   static constexpr int kWavesPerEu = (kWgPerCu * kWaves) / 4 > 1 ? (kWgPerCu * kWaves) / 4 : 1;
-  static_assert(kChunks % kWaves == 0, "page chunks must split evenly over the waves");
 };
 
-// Direct global -> LDS copy of one page: wave w moves chunks c = u * waves + w (rows 4c .. 4c+3).
-// Lane l fills LDS slot l of the chunk (row 4c + l/16, stored slot l%16) with the global slot that
-// the layout puts there. The page offset and the chunk offset are scalars.
-template <int BLOCK, int HPW, bool IS_K>
+// Direct global -> LDS copy of one page by NW waves: wave w moves chunks c = u * NW + w (rows
+// 4c .. 4c+3). Lane l fills LDS slot l of the chunk (row 4c + l/16, stored slot l%16) with the
+// global slot that the layout puts there. The page offset and the chunk offset are scalars.
+template <int BLOCK, int NW, bool IS_K>
 __device__ __forceinline__ void copy_page(__amdgpu_buffer_rsrc_t rs, char* dst, int page_off,
                                           int w, int lane) {
-  using Cfg = TileCfg<BLOCK, HPW>;
+  constexpr int kChunks = BLOCK * kHeadDim * 2 / 1024;
+  static_assert(kChunks % NW == 0, "page chunks must split evenly over the waves");
+  // The wave's first chunk in LDS and in the page. Kept opaque so that the per-chunk addresses are
+  // formed here (one scalar add each) instead of being held in registers across the page loop.
+  int lds0 = (int)(size_t)COSA_LDS(dst) + w * 1024;
+  int src0 = page_off + w * 1024;
+  asm volatile("" : "+s"(lds0), "+s"(src0));
 #pragma unroll
-  for (int u = 0; u < Cfg::kChunksPerWave; ++u) {
-    const int c = u * Cfg::kWaves + w;
+  for (int u = 0; u < kChunks / NW; ++u) {
+    const int c = u * NW + w;
     const int row = 4 * c + (lane >> 4);
     const int stored = lane & 15;
     const int slot = IS_K ? (stored ^ (row & 15)) : (stored ^ ((row & 3) << 2));
     const int voff = (lane >> 4) * (kHeadDim * 2) + slot * 16;
-    __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, COSA_LDS(dst + c * 1024), 16, voff,
-                                             page_off + c * 1024, 0, 0);
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(
+        rs, (__attribute__((address_space(3))) void*)(size_t)(lds0 + u * NW * 1024), 16, voff,
+        src0 + u * NW * 1024, 0, 0);
   }
 }
 
@@ -99,7 +111,8 @@ void attention_kernel(const AttnParams P) {
   const int i = P.nb - 1 - (unit % P.nb);  // heaviest query blocks first
   const int ng = unit / P.nb;              // n * Hkv + g
   const int g = ng % P.Hkv, n = ng / P.Hkv;
-  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int w = __builtin_amdgcn_readfirstlane(tid >> 6);  // wave index, scalar
   const int half = lane >> 5, l32 = lane & 31;
   const int hw = w / WPH, wl = w % WPH;  // head slot in the workgroup, wave within the head
   const int h = g * P.G + pair * HPW + hw;
@@ -129,15 +142,14 @@ void attention_kernel(const AttnParams P) {
   };
   auto page_of = [&](int raw) -> int { return (unsigned)raw <= (unsigned)i ? raw : i; };
 
-  // Prologue: K and V of page 0, K of page 1.
-  int raw0 = __builtin_amdgcn_readfirstlane(raw_entry(0));
-  int raw1 = __builtin_amdgcn_readfirstlane(raw_entry(1));
-  int raw2 = raw_entry(2);  // becomes scalar after the first barrier
+  // Prologue: K and V of page 0.
+  const int raw0 = __builtin_amdgcn_readfirstlane(raw_entry(0));
+  const int raw1 = __builtin_amdgcn_readfirstlane(raw_entry(1));
+  const int raw2 = raw_entry(2);
   if (cnt > 0) {
-    copy_page<BLOCK, HPW, true>(krs, k_lds0, page_of(raw0) * PAGE, w, lane);
-    copy_page<BLOCK, HPW, false>(vrs, v_lds0, page_of(raw0) * PAGE, w, lane);
+    copy_page<BLOCK, Cfg::kWaves, true>(krs, k_lds0, page_of(raw0) * PAGE, w, lane);
+    copy_page<BLOCK, Cfg::kWaves, false>(vrs, v_lds0, page_of(raw0) * PAGE, w, lane);
   }
-  if (cnt > 1) copy_page<BLOCK, HPW, true>(krs, k_lds1, page_of(raw1) * PAGE, w, lane);
 
   // Q^T as the MFMA B operand: lane owns query row qrow, 8 chunks of 16 d (8 per lane half).
   bf16x8_t qf[8];
@@ -172,25 +184,27 @@ void attention_kernel(const AttnParams P) {
   }
   const size_t log_off = ((size_t)(n * P.Hq + h) * P.nb + i) * P.nb;
   int ncomp = 0;
-  int j_cur = page_of(raw0);
-  bool v_cur = OSK ? ((unsigned)raw0 <= (unsigned)i) : true;
-  int raw_a = raw1;  // entry m+1 (scalar)
+  // List entries of the phase's page m (cur) and m+1 (nxt), scalar; pre holds entry m+2 in flight.
+  int cur = raw0, nxt = raw1;
+  int pre = raw2;
 
-  __builtin_amdgcn_s_waitcnt(0);  // prologue pages and Q fragments
+  __builtin_amdgcn_s_waitcnt(0);  // prologue pages, list entries and Q fragments
   __syncthreads();
 
-  // One page of the walk. BUF selects the LDS buffers at compile time, so that every LDS access
-  // names one fixed array: reads of this page's buffers never wait for the in-flight copies into
-  // the other ones, and buffer offsets fold into instruction immediates.
-  auto step = [&](int kk, auto bufc) {
+  // State handed from QK(m) to PV(m) of the same wave.
+  f32x16_t s[KT];
+  float mnew = -INFINITY;
+  bool v_pend = false;  // page m is a valid entry
+
+  // QK(m) on K buffer BUF.
+  auto qk_half = [&](auto bufc) __attribute__((always_inline)) {
     constexpr int BUF = decltype(bufc)::value;
     const char* Kb = BUF ? k_lds1 : k_lds0;
-    const char* Vb = BUF ? v_lds1 : v_lds0;
-
+    const int j = page_of(cur);
+    v_pend = OSK ? ((unsigned)cur <= (unsigned)i) : true;
     // S^T tile t: keys 32 t + 8 (r / 4) + 4 half + r % 4 (register r) of query row qrow. The d chunk
     // is the outer loop: the KT tiles are independent accumulation chains, and each chunk's KT
     // fragments are read from LDS as one batch.
-    f32x16_t s[KT];
 #pragma unroll
     for (int t = 0; t < KT; ++t)
 #pragma unroll
@@ -206,16 +220,23 @@ void attention_kernel(const AttnParams P) {
       __builtin_amdgcn_sched_group_barrier(0x100, KT, 0);  // the chunk's LDS reads ...
       __builtin_amdgcn_sched_group_barrier(0x008, KT, 0);  // ... then its MFMAs
     }
-    if (j_cur == i) {  // diagonal block: causal mask inside the tile
+    if (j == i) {  // diagonal block: causal mask inside the tile
       // key 32 t + 8 (r / 4) + 4 half + r % 4 > query wl*32 + l32, with the lane part moved to the
       // right-hand side so that every compare is against an immediate
+      // (the sign of qh - key selects -inf bit by bit, so no compare masks are kept in registers)
       int qh = wl * 32 + l32 - 4 * half;
       asm volatile("" : "+v"(qh));
 #pragma unroll
       for (int t = 0; t < KT; ++t)
 #pragma unroll
-        for (int r = 0; r < 16; ++r)
-          if (32 * t + 8 * (r >> 2) + (r & 3) > qh) s[t][r] = -INFINITY;
+        for (int r = 0; r < 16; ++r) {
+          int d = qh - (32 * t + 8 * (r >> 2) + (r & 3));
+          asm volatile("" : "+v"(d));
+          const uint32_t masked = (uint32_t)(d >> 31);  // all ones where key > query
+          const float sv = s[t][r];  // bit_cast of a vector element itself reads element 0
+          const uint32_t bits = __builtin_bit_cast(uint32_t, sv);
+          s[t][r] = __builtin_bit_cast(float, (bits & ~masked) | (0xFF800000u & masked));
+        }
     }
     float mloc = -INFINITY;
 #pragma unroll
@@ -223,26 +244,21 @@ void attention_kernel(const AttnParams P) {
 #pragma unroll
       for (int r = 0; r < 16; ++r) mloc = fmaxf(mloc, s[t][r]);
     mloc = fmaxf(mloc, swap_halves(mloc));
-    const float mnew = v_cur ? fmaxf(m, mloc) : m;
+    mnew = v_pend ? fmaxf(m, mloc) : m;
     if constexpr (OSK) {
       // Eq. (skip): each head's b-row tile votes with its largest (m_loc - m), in nats.
       const float marg = wave_max((mloc - mnew) * P.scale);
       if (lane == 0) vote[BUF][w] = marg;
     }
-    __builtin_amdgcn_s_waitcnt(0);  // V of page m and K of page m+1 have landed (this wave's part)
-    __syncthreads();
+  };
 
-    // Pages m+1 (V) and m+2 (K) can now be overwritten by their successors.
-    const int raw_b = __builtin_amdgcn_readfirstlane(raw2);  // entry m+2
-    raw2 = raw_entry(kk + 3);
-    if (kk + 1 < cnt)
-      copy_page<BLOCK, HPW, false>(vrs, BUF ? v_lds0 : v_lds1, page_of(raw_a) * PAGE, w, lane);
-    if (kk + 2 < cnt)
-      copy_page<BLOCK, HPW, true>(krs, BUF ? k_lds1 : k_lds0, page_of(raw_b) * PAGE, w, lane);
-
-    bool skip = !v_cur;
+  // PV(kk) on V buffer BUF: the votes of this head's waves were posted in the previous phase.
+  auto pv_half = [&](int kk, auto bufc) __attribute__((always_inline)) {
+    constexpr int BUF = decltype(bufc)::value;
+    const char* Vb = BUF ? v_lds1 : v_lds0;
+    bool skip = !v_pend;
     if constexpr (OSK) {
-      if (v_cur) {
+      if (v_pend) {
         float dk = vote[BUF][hw * WPH];
 #pragma unroll
         for (int ww = 1; ww < WPH; ++ww) dk = fmaxf(dk, vote[BUF][hw * WPH + ww]);
@@ -300,15 +316,49 @@ void attention_kernel(const AttnParams P) {
       }
       ++ncomp;
     }
-    j_cur = page_of(raw_a);
-    v_cur = OSK ? ((unsigned)raw_a <= (unsigned)i) : true;
-    raw_a = raw_b;
   };
 
+  // End of a phase: LDS writes done (and, with full, this wave's page copies landed), then the
+  // workgroup barrier. The compiler barriers keep LDS accesses on their side of it.
+  auto end_phase = [&](bool full) __attribute__((always_inline)) {
+    if (full)
+      __builtin_amdgcn_s_waitcnt(kVmcntLgkm0);
+    else
+      __builtin_amdgcn_s_waitcnt(kLgkm0);
+    asm volatile("" ::: "memory");
+    __builtin_amdgcn_s_barrier();
+    asm volatile("" ::: "memory");
+  };
+
+  // Page kk, its buffers BUF: fetch page kk+1 into the other buffers, QK, barrier, PV, barrier.
+  auto page = [&](int kk, auto bufc) __attribute__((always_inline)) {
+    constexpr int BUF = decltype(bufc)::value;
+    pre = raw_entry(kk + 2);
+    if (kk + 1 < cnt) {
+      const int off = page_of(nxt) * PAGE;
+      if constexpr (HPW == 1) {
+        copy_page<BLOCK, WPH, true>(krs, BUF ? k_lds0 : k_lds1, off, wl, lane);
+        copy_page<BLOCK, WPH, false>(vrs, BUF ? v_lds0 : v_lds1, off, wl, lane);
+      } else if (hw == 0) {
+        copy_page<BLOCK, WPH, true>(krs, BUF ? k_lds0 : k_lds1, off, wl, lane);
+      } else {
+        copy_page<BLOCK, WPH, false>(vrs, BUF ? v_lds0 : v_lds1, off, wl, lane);
+      }
+    }
+    qk_half(bufc);
+    end_phase(false);
+    pv_half(kk, bufc);
+    end_phase(true);
+    cur = nxt;
+    nxt = __builtin_amdgcn_readfirstlane(pre);
+  };
+
+  if (HPW == 2 && hw == 1) end_phase(false);  // head slot 1 runs one phase behind
   for (int kk = 0; kk < cnt; kk += 2) {
-    step(kk, std::integral_constant<int, 0>{});
-    if (kk + 1 < cnt) step(kk + 1, std::integral_constant<int, 1>{});
+    page(kk, std::integral_constant<int, 0>{});
+    if (kk + 1 < cnt) page(kk + 1, std::integral_constant<int, 1>{});
   }
+  if (HPW == 2 && hw == 0) end_phase(false);  // same barrier count for both head slots
 
   lsum += swap_halves(lsum);
   const float inv = lsum > 0.f ? 1.f / lsum : 0.f;
