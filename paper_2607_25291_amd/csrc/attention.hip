@@ -243,7 +243,7 @@ void attention_kernel(const AttnParams P) {
     for (int t = 0; t < KT; ++t)
 #pragma unroll
       for (int r = 0; r < 16; ++r) mloc = fmaxf(mloc, s[t][r]);
-    mloc = fmaxf(mloc, swap_halves(mloc));
+    mloc = half_max(mloc);
     mnew = v_pend ? fmaxf(m, mloc) : m;
     if constexpr (OSK) {
       // Eq. (skip): each head's b-row tile votes with its largest (m_loc - m), in nats.
@@ -360,7 +360,7 @@ void attention_kernel(const AttnParams P) {
   }
   if (HPW == 2 && hw == 0) end_phase(false);  // same barrier count for both head slots
 
-  lsum += swap_halves(lsum);
+  lsum = half_sum(lsum);
   const float inv = lsum > 0.f ? 1.f / lsum : 0.f;
   uint16_t* op = P.a.o + qo_off + (size_t)qrow * kHeadDim;
 #pragma unroll

@@ -29,14 +29,54 @@ __device__ __forceinline__ bf16x8_t as_bf16x8(const u32x4_t& v) {
   return __builtin_bit_cast(bf16x8_t, v);
 }
 
-__device__ __forceinline__ float wave_max(float v) {
-#pragma unroll
-  for (int off = 32; off >= 1; off >>= 1) v = fmaxf(v, __shfl_xor(v, off));
+// Cross-lane reductions without the LDS crossbar (ds_bpermute costs an LDS round trip per step):
+// v_permlane32_swap exchanges the two 32-lane halves, DPP moves data within rows of 16 lanes, and
+// v_readlane takes the last step into a scalar.
+
+// Both halves' values of each lane pair (l, l ^ 32): lo gets lane l % 32, hi lane l % 32 + 32.
+__device__ __forceinline__ void half_pair(float v, float& lo, float& hi) {
+  const unsigned u = __builtin_bit_cast(unsigned, v);
+  const auto r = __builtin_amdgcn_permlane32_swap(u, u, false, false);
+  const unsigned a = r[0], b = r[1];
+  lo = __builtin_bit_cast(float, a);
+  hi = __builtin_bit_cast(float, b);
+}
+
+// max / sum of v over the lane pair (l, l ^ 32), the same in both lanes.
+__device__ __forceinline__ float half_max(float v) {
+  float lo, hi;
+  half_pair(v, lo, hi);
+  return fmaxf(lo, hi);
+}
+__device__ __forceinline__ float half_sum(float v) {
+  float lo, hi;
+  half_pair(v, lo, hi);
+  return lo + hi;
+}
+
+template <int CTRL>
+__device__ __forceinline__ float dpp_mov(float v) {
+  const int u = __builtin_bit_cast(int, v);
+  const int r = __builtin_amdgcn_update_dpp(u, u, CTRL, 0xF, 0xF, false);
+  return __builtin_bit_cast(float, r);
+}
+
+// max of v over each row of 16 lanes, in every lane of the row.
+__device__ __forceinline__ float row16_max(float v) {
+  v = fmaxf(v, dpp_mov<0xB1>(v));   // quad_perm [1,0,3,2]
+  v = fmaxf(v, dpp_mov<0x4E>(v));   // quad_perm [2,3,0,1]
+  v = fmaxf(v, dpp_mov<0x141>(v));  // row_half_mirror: lane i <- 7 - i within 8
+  v = fmaxf(v, dpp_mov<0x140>(v));  // row_mirror: lane i <- 15 - i within 16
   return v;
 }
 
-// Exchange with the lane 32 apart (the other half of the wave).
-__device__ __forceinline__ float swap_halves(float v) { return __shfl_xor(v, 32); }
+// max of v over the wave, as a wave-uniform value.
+__device__ __forceinline__ float wave_max(float v) {
+  v = row16_max(half_max(v));  // rows 0 and 1 now cover lanes {0-15, 32-47} and {16-31, 48-63}
+  const int a = __builtin_amdgcn_readlane(__builtin_bit_cast(int, v), 0);
+  const int b = __builtin_amdgcn_readlane(__builtin_bit_cast(int, v), 16);
+  return fmaxf(__builtin_bit_cast(float, a), __builtin_bit_cast(float, b));
+}
 
 // XCD-aware tile mapping. Workgroup ids are dealt round-robin to the 8 XCDs, so workgroup p runs on
 // XCD p % 8. Tiles are grouped in units of G (the query heads that share one KV head and one list):

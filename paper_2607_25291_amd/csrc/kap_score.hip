@@ -107,7 +107,7 @@ __global__ __launch_bounds__(kScoreThreads) void kap_score_kernel(const KapParam
         for (int q4 = 0; q4 < 4; ++q4) {
           float bm = fmaxf(fmaxf(acc[4 * q4], acc[4 * q4 + 1]),
                            fmaxf(acc[4 * q4 + 2], acc[4 * q4 + 3]));
-          bm = fmaxf(bm, swap_halves(bm));
+          bm = half_max(bm);
           const int j = chunk * 4 + q4;
           if (row_ok && j <= i && (q4 >> 1) == half) brow[j] = bm;
         }
@@ -117,7 +117,7 @@ __global__ __launch_bounds__(kScoreThreads) void kap_score_kernel(const KapParam
           float bm = acc[8 * b2];
 #pragma unroll
           for (int r = 1; r < 8; ++r) bm = fmaxf(bm, acc[8 * b2 + r]);
-          bm = fmaxf(bm, swap_halves(bm));
+          bm = half_max(bm);
           const int j = chunk * 2 + b2;
           if (row_ok && j <= i && b2 == half) brow[j] = bm;
         }
@@ -125,7 +125,7 @@ __global__ __launch_bounds__(kScoreThreads) void kap_score_kernel(const KapParam
         float bm = acc[0];
 #pragma unroll
         for (int r = 1; r < 16; ++r) bm = fmaxf(bm, acc[r]);
-        bm = fmaxf(bm, swap_halves(bm));
+        bm = half_max(bm);
         const int j = chunk;
         if (row_ok && j <= i && half == 0) brow[j] = bm;
       }
