@@ -3,9 +3,9 @@
 // One workgroup (8 wavefronts) per (batch n, KV head g, query block i). Its R = G * spb sampled query
 // rows (tokens (i*spb + t) * s of the G heads of group g) stay in registers as the MFMA B operand.
 // The waves stride over chunks of 32 sampled keys c < (i+1)*spb (tokens c * s), computing the
-// transposed logits K~ Q~^T with bf16 MFMA 32x32x16, applying sm_scale and the causal mask over
-// sampled positions (c <= r), and reducing them straight into per-block maxima beta[row][j] held in
-// LDS. The softmax -> MaxPool -> MaxNorm chain collapses to Pbar = exp(beta - mu) with mu the row
+// transposed logits K~ Q~^T with bf16 MFMA 32x32x16, applying the causal mask over sampled
+// positions (c <= r) and sm_scale, and reducing them straight into per-block maxima beta[row][j] held
+// in LDS. The softmax -> MaxPool -> MaxNorm chain collapses to Pbar = exp(beta - mu) with mu the row
 // maximum (the softmax normaliser cancels in the MaxNorm ratio, exp is monotone), so the score matrix
 // is never materialised. A second phase takes mu per row and, per key block j, sums
 // exp(beta - mu) over the rows in a fixed order (deterministic) and raises the HRM flag when some
@@ -60,7 +60,7 @@ __global__ __launch_bounds__(kScoreThreads) void kap_score_kernel(const KapParam
   }
 
   const uint16_t* kbase = P.a.k + (size_t)ng * P.L * kHeadDim + 8 * half;
-  auto load_keys = [&](int chunk, bf16x8_t (&kf)[8]) {
+  auto load_keys = [&](int chunk, bf16x8_t (&kf)[8]) __attribute__((always_inline)) {
     const int c = chunk * 32 + l32;
     if (chunk < nchunks && c < nkeys) {
       const uint16_t* kp = kbase + (size_t)c * P.s * kHeadDim;
@@ -72,26 +72,28 @@ __global__ __launch_bounds__(kScoreThreads) void kap_score_kernel(const KapParam
     }
   };
 
-  bf16x8_t kcur[8], knext[8];
-  load_keys(w, kcur);
-  for (int chunk = w; chunk < nchunks; chunk += kScoreWaves) {
-    load_keys(chunk + kScoreWaves, knext);  // prefetch
+  auto process = [&](int chunk, const bf16x8_t (&kf)[8]) __attribute__((always_inline)) {
 #pragma unroll
     for (int rt = 0; rt < RT; ++rt) {
       f32x16_t acc;
 #pragma unroll
       for (int r = 0; r < 16; ++r) acc[r] = 0.f;
 #pragma unroll
-      for (int cc = 0; cc < 8; ++cc) acc = mfma32x32x16(kcur[cc], qf[rt][cc], acc);
-      // acc[r]: sampled key chunk*32 + 8 (r/4) + 4 half + r%4, row rt*32 + l32.
+      for (int cc = 0; cc < 8; ++cc) acc = mfma32x32x16(kf[cc], qf[rt][cc], acc);
+      // acc[r]: sampled key chunk*32 + 8 (r/4) + 4 half + r%4, row rt*32 + l32. Only a chunk that
+      // reaches block i (or the zero-filled keys past the last sample) needs the causal mask; the
+      // branch is uniform over the wave.
       const int row = rt * 32 + l32;
-      const int rs = i * SPB + (row % SPB);
+      if (chunk * 32 + 31 > i * SPB) {
+        const int rs = i * SPB + (row % SPB);
 #pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const int key = chunk * 32 + 8 * (r >> 2) + 4 * half + (r & 3);
-        const float v = acc[r] * P.scale;
-        acc[r] = key > rs ? -INFINITY : v;
+        for (int r = 0; r < 16; ++r) {
+          const int key = chunk * 32 + 8 * (r >> 2) + 4 * half + (r & 3);
+          acc[r] = key > rs ? -INFINITY : acc[r];
+        }
       }
+      // Block maxima are taken on the raw logits and scaled once: x -> sm_scale * x is monotone
+      // under rounding, so the scaled maximum equals the maximum of the scaled logits exactly.
       const bool row_ok = row < P.R;
       float* brow = beta + row * P.nbp;
       if constexpr (SPB == 4) {
@@ -100,7 +102,7 @@ __global__ __launch_bounds__(kScoreThreads) void kap_score_kernel(const KapParam
           const float bm = fmaxf(fmaxf(acc[4 * q4], acc[4 * q4 + 1]),
                                  fmaxf(acc[4 * q4 + 2], acc[4 * q4 + 3]));
           const int j = chunk * 8 + 2 * q4 + half;
-          if (row_ok && j <= i) brow[j] = bm;
+          if (row_ok && j <= i) brow[j] = bm * P.scale;
         }
       } else if constexpr (SPB == 8) {
 #pragma unroll
@@ -109,7 +111,7 @@ __global__ __launch_bounds__(kScoreThreads) void kap_score_kernel(const KapParam
                            fmaxf(acc[4 * q4 + 2], acc[4 * q4 + 3]));
           bm = half_max(bm);
           const int j = chunk * 4 + q4;
-          if (row_ok && j <= i && (q4 >> 1) == half) brow[j] = bm;
+          if (row_ok && j <= i && (q4 >> 1) == half) brow[j] = bm * P.scale;
         }
       } else if constexpr (SPB == 16) {
 #pragma unroll
@@ -119,7 +121,7 @@ __global__ __launch_bounds__(kScoreThreads) void kap_score_kernel(const KapParam
           for (int r = 1; r < 8; ++r) bm = fmaxf(bm, acc[8 * b2 + r]);
           bm = half_max(bm);
           const int j = chunk * 2 + b2;
-          if (row_ok && j <= i && b2 == half) brow[j] = bm;
+          if (row_ok && j <= i && b2 == half) brow[j] = bm * P.scale;
         }
       } else {
         float bm = acc[0];
@@ -127,9 +129,16 @@ __global__ __launch_bounds__(kScoreThreads) void kap_score_kernel(const KapParam
         for (int r = 1; r < 16; ++r) bm = fmaxf(bm, acc[r]);
         bm = half_max(bm);
         const int j = chunk;
-        if (row_ok && j <= i && half == 0) brow[j] = bm;
+        if (row_ok && j <= i && half == 0) brow[j] = bm * P.scale;
       }
     }
+  };
+  // The next chunk of this wave is loaded while the current one is processed.
+  bf16x8_t kcur[8], knext[8];
+  load_keys(w, kcur);
+  for (int chunk = w; chunk < nchunks; chunk += kScoreWaves) {
+    load_keys(chunk + kScoreWaves, knext);
+    process(chunk, kcur);
 #pragma unroll
     for (int cc = 0; cc < 8; ++cc) kcur[cc] = knext[cc];
   }
