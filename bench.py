@@ -1,6 +1,7 @@
 """Benchmark of CoSA prefill attention (KAP + OSK) on one MI355X, against the in-house dense kernel.
 
     python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload qwen3_8b_l128k]
+    python bench.py --sweep [--steps K]     # budget / visiting-order sweep (one JSON object)
 
 A step is one pass of the whole hot path, cosa_prefill (proxy scoring, ordered selection, ordered-
 skipping attention) over one attention layer of synthetic bf16 inputs that are already resident in
@@ -119,6 +120,105 @@ def cpu_baseline(w, q, k, v, gpu_count, gpu_ncomp, delta, budget_s: float = 15.0
                        "cost model (proxy unit ~ i+1 keys, OSK tile ~ listed + computed blocks)")}
 
 
+def run_sweep(args):
+    """Budget and visiting-order sweep on one workload (default 128K).
+
+    Grid: stage-1 budget B1 in {5, 10, 20, 40} % times overall budget B2 in {1, 1/2, 1/4} * B1.
+    For each point: KAP order with Delta calibrated to B2; ascending order with that same Delta;
+    ascending order with Delta recalibrated to B2. B2 = B1 runs with skipping off. Each record has
+    the cosa_prefill latency, the realized budgets and the output error against the dense kernel
+    on the same inputs (all on the GPU).
+    """
+    import torch
+    from paper_2607_25291_amd import binding as B
+    from paper_2607_25291_amd.calibrate import delta_for_budget
+    from paper_2607_25291_amd.inputs import WORKLOADS, make_inputs
+
+    w = WORKLOADS[args.workload]
+    dev = torch.device("cuda:0")
+    stream = torch.cuda.current_stream()
+    p = B.Problem(w.batch, w.n_q_heads, w.n_kv_heads, w.seq_len, w.head_dim, w.block, w.stride)
+    nb, G = w.n_blocks, w.n_q_heads // w.n_kv_heads
+    log(f"[sweep] {w.name}: generating inputs")
+    q_np, k_np, v_np = make_inputs(w)
+    up = lambda a: torch.from_numpy(a.view(np.int16)).to(dev)
+    q, k, v = up(q_np), up(k_np), up(v_np)
+    o = torch.empty_like(q)
+    o_dense = torch.empty_like(q)
+    nbytes = B.cosa_prefill_workspace_bytes(p)
+    ws = torch.zeros(nbytes, dtype=torch.uint8, device=dev)
+    lay = B.cosa_prefill_workspace_layout(p)
+    cells = w.batch * w.n_kv_heads * nb * nb
+    score = ws[lay.score:lay.score + 4 * cells].view(torch.float32)
+    hrm = ws[lay.hrm:lay.hrm + cells]
+    order = ws[lay.order:lay.order + 4 * cells].view(torch.int32)
+    count = ws[lay.count:lay.count + 4 * w.batch * w.n_kv_heads * nb].view(torch.int32)
+    margin = torch.zeros((w.batch, w.n_q_heads, nb, nb), dtype=torch.float32, device=dev)
+    total = w.batch * w.n_q_heads * nb * (nb + 1) // 2
+    B.cosa_dense_attention(p, q, k, v, o_dense)
+    dense_f = o_dense.view(torch.bfloat16).float()
+
+    def lists(sel):
+        B.cosa_kap_score(p, q, k, score, hrm)
+        B.cosa_kap_select_ordered(p, score, hrm, sel, order, count)
+        cnt_q = np.repeat(count.view(w.batch, w.n_kv_heads, nb).cpu().numpy(), G, axis=1)
+        return cnt_q, int(cnt_q.sum())
+
+    def margins(cnt_q):
+        margin.zero_()
+        B.cosa_osk_attention(p, q, k, v, order, count, None, o, None, margin, None)
+        pos = np.arange(nb)[None, None, None, :] < cnt_q[..., None]
+        return margin.cpu().numpy()[pos]
+
+    def measure(sel, sk, listed):
+        ncomp = torch.zeros((w.batch, w.n_q_heads, nb), dtype=torch.int32, device=dev)
+        B.cosa_osk_attention(p, q, k, v, order, count, sk, o, None, None, ncomp)
+        computed = int(ncomp.sum())
+        for _ in range(2):
+            B.cosa_prefill(p, q, k, v, sel, sk, ws, nbytes, o)
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        for _ in range(args.steps):
+            B.cosa_prefill(p, q, k, v, sel, sk, ws, nbytes, o)
+        e1.record(stream)
+        torch.cuda.synchronize()
+        diff = (o.view(torch.bfloat16).float() - dense_f).abs()
+        return {"ms": round(e0.elapsed_time(e1) / args.steps, 4),
+                "realized_b1": round(listed / total, 5), "realized_b": round(computed / total, 5),
+                "err_max": round(float(diff.max()), 5), "err_mean": round(float(diff.mean()), 6)}
+
+    recs = []
+    for b1 in (0.05, 0.10, 0.20, 0.40):
+        for frac in (1.0, 0.5, 0.25):
+            b2 = b1 * frac
+            sel_k = B.select(B.SELECT_FRACTION, b1, B.ORDER_KAP)
+            sel_a = B.select(B.SELECT_FRACTION, b1, B.ORDER_ASCENDING)
+            cnt_q, listed = lists(sel_k)
+            if frac == 1.0:
+                sk_k = sk_same = B.skip(B.SKIP_NONE, 0.0)
+                delta_k = None
+            else:
+                delta_k, _, _ = delta_for_budget(margins(cnt_q), listed, total, b2, w.seq_len)
+                sk_k = sk_same = B.skip(B.SKIP_ROWMAX, delta_k)
+            r = measure(sel_k, sk_k, listed)
+            recs.append({"b1": b1, "b2_target": b2, "order": "kap", "delta": delta_k, **r})
+            log(f"[sweep] B1 {b1:.2f} B2 {b2:.4f} kap: {r}")
+            cnt_a, listed_a = lists(sel_a)
+            r = measure(sel_a, sk_same, listed_a)
+            recs.append({"b1": b1, "b2_target": b2, "order": "ascending", "delta_from": "kap",
+                         "delta": delta_k, **r})
+            log(f"[sweep] B1 {b1:.2f} B2 {b2:.4f} ascending, same delta: {r}")
+            if frac != 1.0:
+                delta_a, _, _ = delta_for_budget(margins(cnt_a), listed_a, total, b2, w.seq_len)
+                r = measure(sel_a, B.skip(B.SKIP_ROWMAX, delta_a), listed_a)
+                recs.append({"b1": b1, "b2_target": b2, "order": "ascending",
+                             "delta_from": "recalibrated", "delta": delta_a, **r})
+                log(f"[sweep] B1 {b1:.2f} B2 {b2:.4f} ascending, recalibrated delta: {r}")
+    print(json.dumps({"workload": w.name, "steps": args.steps, "data": "synthetic",
+                      "records": recs}), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -127,6 +227,8 @@ def main():
     ap.add_argument("--workload", default="qwen3_8b_l128k")
     ap.add_argument("--dense-steps", type=int, default=3)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--sweep", action="store_true",
+                    help="run the budget / visiting-order sweep instead of the one-line benchmark")
     ap.add_argument("--copy-probe-mib", type=int, default=0,
                     help="run one plain device copy of this many MiB first (counter calibration)")
     args = ap.parse_args()
@@ -135,6 +237,9 @@ def main():
               "multi-GPU sharding of this path is a design note, not an implemented mode.",
               file=sys.stderr)
         sys.exit(2)
+    if args.sweep:
+        run_sweep(args)
+        return
 
     import torch
     from paper_2607_25291_amd import binding as B
