@@ -227,6 +227,9 @@ def main():
     ap.add_argument("--workload", default="qwen3_8b_l128k")
     ap.add_argument("--dense-steps", type=int, default=3)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--page-size", type=int, default=0,
+                    help="time cosa_prefill_paged on a paged KV cache with this page size "
+                         "(pages placed by a random permutation); 0: contiguous K/V")
     ap.add_argument("--sweep", action="store_true",
                     help="run the budget / visiting-order sweep instead of the one-line benchmark")
     ap.add_argument("--copy-probe-mib", type=int, default=0,
@@ -268,6 +271,27 @@ def main():
     order = ws[lay.order:lay.order + 4 * cells].view(torch.int32)
     count = ws[lay.count:lay.count + 4 * w.batch * w.n_kv_heads * nb].view(torch.int32)
     sel = B.select(B.SELECT_FRACTION, w.kap_budget)
+    kv = None
+    if args.page_size:
+        # the same K/V placed in a paged cache [n_pages, Hkv, page, d] through a random table
+        ps = args.page_size
+        per_seq = w.seq_len // ps
+        n_pages = w.batch * per_seq + 8
+        perm = torch.from_numpy(np.random.default_rng(123).permutation(n_pages).astype(np.int32))
+        table = perm[:w.batch * per_seq].view(w.batch, per_seq).to(dev)
+        kc = torch.zeros((n_pages, w.n_kv_heads, ps, w.head_dim), dtype=torch.int16, device=dev)
+        vc = torch.zeros_like(kc)
+        for n in range(w.batch):
+            kc[table[n].long()] = k[n].view(w.n_kv_heads, per_seq, ps, w.head_dim).transpose(0, 1)
+            vc[table[n].long()] = v[n].view(w.n_kv_heads, per_seq, ps, w.head_dim).transpose(0, 1)
+        kv = B.paged_kv(kc, vc, table, ps, n_pages)
+        log(f"[bench] paged KV cache: page {ps}, {n_pages} pages")
+
+    def prefill_step():
+        if kv is None:
+            B.cosa_prefill(p, q, k, v, sel, sk, ws, nbytes, o)
+        else:
+            B.cosa_prefill_paged(p, q, kv, sel, sk, ws, nbytes, o)
 
     if args.copy_probe_mib:
         src = torch.empty(args.copy_probe_mib * 2 ** 20 // 4, dtype=torch.float32, device=dev)
@@ -301,13 +325,13 @@ def main():
 
     # ---- timed region: K steps of the whole hot path ----
     for _ in range(args.warmup):
-        B.cosa_prefill(p, q, k, v, sel, sk, ws, nbytes, o)
+        prefill_step()
     torch.cuda.synchronize()
     ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     t_wall = time.perf_counter()
     ev0.record(stream)
     for _ in range(args.steps):
-        B.cosa_prefill(p, q, k, v, sel, sk, ws, nbytes, o)
+        prefill_step()
     ev1.record(stream)
     torch.cuda.synchronize()
     wall = time.perf_counter() - t_wall
@@ -318,11 +342,17 @@ def main():
     evs = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(args.steps)]
     for e in evs:
         e[0].record(stream)
-        B.cosa_kap_score(p, q, k, score, hrm)
+        if kv is None:
+            B.cosa_kap_score(p, q, k, score, hrm)
+        else:
+            B.cosa_kap_score_paged(p, q, kv, score, hrm)
         e[1].record(stream)
         B.cosa_kap_select_ordered(p, score, hrm, sel, order, count)
         e[2].record(stream)
-        B.cosa_osk_attention(p, q, k, v, order, count, sk, o, None, None, None)
+        if kv is None:
+            B.cosa_osk_attention(p, q, k, v, order, count, sk, o, None, None, None)
+        else:
+            B.cosa_osk_attention_paged(p, q, kv, order, count, sk, o, None, None, None)
         e[3].record(stream)
     torch.cuda.synchronize()
     st = np.array([[e[a].elapsed_time(e[a + 1]) for a in range(3)] for e in evs])
@@ -355,7 +385,7 @@ def main():
     dense_tflops = f_dense / (t_dense * 1e-3) / 1e12 if t_dense else None
     kf, kb = kap_score_work(w.batch, w.n_q_heads, w.n_kv_heads, nb, w.block, w.stride,
                             w.head_dim)
-    traffic = traffic_from_profile("osk_attention", "attention.hip")
+    traffic = None if args.page_size else traffic_from_profile("osk_attention", "attention.hip")
 
     cpu = None
     if not args.no_cpu_baseline:
@@ -379,6 +409,8 @@ def main():
                    "n_kv_heads": w.n_kv_heads, "seq_len": w.seq_len, "head_dim": w.head_dim,
                    "block": w.block, "stride": w.stride, "kap_budget": w.kap_budget,
                    "osk_budget": w.osk_budget, "select": "fraction", "delta": round(delta, 4),
+                   "kv_layout": (f"paged, page {args.page_size}" if args.page_size
+                                 else "contiguous"),
                    "parallelism": "single GPU"},
         "speedup_vs_dense": round(t_dense / ms_step, 3) if t_dense else None,
         "dense_ms_per_layer": round(t_dense, 3) if t_dense else None,

@@ -30,6 +30,10 @@
  * Supported problem space (COSA_ERR_UNSUPPORTED otherwise): head_dim == 128, block in {64, 128},
  * causal == 1, seq_len a multiple of block, samples per block (block / stride) in {4, 8, 16, 32},
  * G * (block / stride) <= 128 rows per proxy unit, and nb <= 8192.
+ *
+ * The *_paged entry points take K and V from a paged KV cache (cosa_paged_kv) instead of the
+ * contiguous [B, Hkv, L, d] tensors; everything else is unchanged, and on the same data their
+ * results are bit-identical to the contiguous calls.
  */
 #ifndef COSA_H_
 #define COSA_H_
@@ -105,6 +109,29 @@ typedef struct {
   size_t total; /* bytes required           */
 } cosa_workspace_layout;
 
+/*
+ * Paged KV cache (Sec. 4.3 "Physical jumping over pages"; Algorithm A takes paged K and V; appendix
+ * D.1: a logical block of b tokens resolves through one or more physical pages when the page size
+ * b_p differs from b). The order invariance of Sec. 3.2 is what lets the walk visit pages in any
+ * order through such a table.
+ *   k_cache, v_cache: bf16 [n_pages, n_kv_heads, page_size, head_dim]; page p of KV head g holds
+ *                     page_size consecutive tokens, each a contiguous row of head_dim values.
+ *   page_table:       int32 [batch, seq_len / page_size]; entry [n, t / page_size] is the physical
+ *                     page holding token t of sequence n (for every KV head).
+ *   page_size:        tokens per page, a power of two in [16, 2^20] that divides seq_len.
+ *   n_pages:          physical pages in each cache (>= 1).
+ * Pointers are device pointers owned by the caller. Table entries are device data and are not
+ * checked before launch: an entry outside [0, n_pages) is read as page 0 (the kernels never read
+ * outside the caches; the affected outputs are then meaningless).
+ */
+typedef struct {
+  const void* k_cache;
+  const void* v_cache;
+  const int32_t* page_table;
+  int32_t page_size;
+  int64_t n_pages;
+} cosa_paged_kv;
+
 /* Human-readable name of a status code (static storage). */
 const char* cosa_status_string(cosa_status status);
 
@@ -177,6 +204,30 @@ cosa_status cosa_prefill_workspace_layout(const cosa_problem* problem,
 cosa_status cosa_prefill(const cosa_problem* problem, const void* q, const void* k, const void* v,
                          const cosa_select* select, const cosa_skip* skip, void* workspace,
                          size_t workspace_bytes, void* o, void* stream);
+
+/*
+ * cosa_kap_score with K read from a paged cache (kv->v_cache is not used and may be NULL):
+ * sampled key c (token c * stride) of KV head g is row (token % page_size) of physical page
+ * page_table[n, token / page_size].
+ */
+cosa_status cosa_kap_score_paged(const cosa_problem* problem, const void* q,
+                                 const cosa_paged_kv* kv, float* score, uint8_t* hrm, void* stream);
+
+/*
+ * cosa_osk_attention with K and V read from a paged cache: the K and V pages of a listed block j
+ * are gathered through page_table (b / page_size physical pages per block when page_size < b, a
+ * part of one page otherwise), in list order.
+ */
+cosa_status cosa_osk_attention_paged(const cosa_problem* problem, const void* q,
+                                     const cosa_paged_kv* kv, const int32_t* order,
+                                     const int32_t* count, const cosa_skip* skip, void* o,
+                                     uint8_t* visit_log, float* margin_log, int32_t* n_computed,
+                                     void* stream);
+
+/* cosa_prefill (Algorithm A end to end) on a paged KV cache; same workspace as cosa_prefill. */
+cosa_status cosa_prefill_paged(const cosa_problem* problem, const void* q, const cosa_paged_kv* kv,
+                               const cosa_select* select, const cosa_skip* skip, void* workspace,
+                               size_t workspace_bytes, void* o, void* stream);
 
 #ifdef __cplusplus
 }

@@ -44,6 +44,12 @@ class CosaWorkspaceLayout(ctypes.Structure):
                 ("count", ctypes.c_size_t), ("total", ctypes.c_size_t)]
 
 
+class CosaPagedKv(ctypes.Structure):
+    _fields_ = [("k_cache", ctypes.c_void_p), ("v_cache", ctypes.c_void_p),
+                ("page_table", ctypes.c_void_p), ("page_size", ctypes.c_int32),
+                ("n_pages", ctypes.c_int64)]
+
+
 class CosaError(RuntimeError):
     def __init__(self, status: int, message: str):
         super().__init__(message)
@@ -110,6 +116,15 @@ def lib():
         L.cosa_prefill.restype = S
         L.cosa_prefill.argtypes = [P, vp, vp, vp, ctypes.POINTER(CosaSelect),
                                    ctypes.POINTER(CosaSkip), vp, ctypes.c_size_t, vp, vp]
+        KV = ctypes.POINTER(CosaPagedKv)
+        L.cosa_kap_score_paged.restype = S
+        L.cosa_kap_score_paged.argtypes = [P, vp, KV, vp, vp, vp]
+        L.cosa_osk_attention_paged.restype = S
+        L.cosa_osk_attention_paged.argtypes = [P, vp, KV, vp, vp, ctypes.POINTER(CosaSkip), vp, vp,
+                                               vp, vp, vp]
+        L.cosa_prefill_paged.restype = S
+        L.cosa_prefill_paged.argtypes = [P, vp, KV, ctypes.POINTER(CosaSelect),
+                                         ctypes.POINTER(CosaSkip), vp, ctypes.c_size_t, vp, vp]
         _lib = L
     return _lib
 
@@ -209,3 +224,36 @@ def cosa_prefill(problem, q, k, v, sel: CosaSelect, sk: Optional[CosaSkip], work
     skp = ctypes.byref(sk) if sk is not None else None
     _check(lib().cosa_prefill(ctypes.byref(p), _ptr(q), _ptr(k), _ptr(v), ctypes.byref(sel), skp,
                               _ptr(workspace), workspace_bytes, _ptr(o), _stream(stream)))
+
+
+def _kvref(kv):
+    return ctypes.byref(kv) if kv is not None else None
+
+
+def paged_kv(k_cache, v_cache, page_table, page_size: int, n_pages: int) -> CosaPagedKv:
+    """cosa_paged_kv from device tensors (v_cache may be None for the proxy-only call)."""
+    return CosaPagedKv(_ptr(k_cache), _ptr(v_cache), _ptr(page_table), page_size, n_pages)
+
+
+def cosa_kap_score_paged(problem, q, kv: CosaPagedKv, score, hrm, stream=None):
+    p = _prob(problem)
+    _check(lib().cosa_kap_score_paged(ctypes.byref(p), _ptr(q), _kvref(kv), _ptr(score),
+                                      _ptr(hrm), _stream(stream)))
+
+
+def cosa_osk_attention_paged(problem, q, kv: CosaPagedKv, order, count, sk: Optional[CosaSkip], o,
+                             visit_log=None, margin_log=None, n_computed=None, stream=None):
+    p = _prob(problem)
+    skp = ctypes.byref(sk) if sk is not None else None
+    _check(lib().cosa_osk_attention_paged(ctypes.byref(p), _ptr(q), _kvref(kv), _ptr(order),
+                                          _ptr(count), skp, _ptr(o), _ptr(visit_log),
+                                          _ptr(margin_log), _ptr(n_computed), _stream(stream)))
+
+
+def cosa_prefill_paged(problem, q, kv: CosaPagedKv, sel: CosaSelect, sk: Optional[CosaSkip],
+                       workspace, workspace_bytes: int, o, stream=None):
+    p = _prob(problem)
+    skp = ctypes.byref(sk) if sk is not None else None
+    _check(lib().cosa_prefill_paged(ctypes.byref(p), _ptr(q), _kvref(kv), ctypes.byref(sel),
+                                    skp, _ptr(workspace), workspace_bytes, _ptr(o),
+                                    _stream(stream)))

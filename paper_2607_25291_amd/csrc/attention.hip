@@ -19,6 +19,9 @@
 // fetch K pages (page m+1 at the start of QK(m)), those of head 1 V pages (page m+1 at the start of
 // their QK(m)); a single head fetches both. A wave waits for its own copies at the end of its PV
 // half, so every copy has two phases to land before the barrier that publishes it.
+// With a paged KV cache (Sec. 4.3 "Physical jumping over pages"; appendix D.1) the copies gather a
+// block's rows through the page table; everything from the LDS layouts on is shared.
+//
 // LDS layouts (one 16-byte slot of 8 values at a time; a direct load writes 64 consecutive slots,
 // each lane picks the global slot that belongs there):
 //   K [key][d]  256-byte rows, slot s of row r stored at slot s ^ (r % 16). The MFMA A-operand reads
@@ -88,7 +91,48 @@ __device__ __forceinline__ void copy_page(__amdgpu_buffer_rsrc_t rs, char* dst, 
   }
 }
 
-template <int BLOCK, int HPW, bool OSK>
+// Paged variant (Sec. 4.3 "Physical jumping over pages"): the block's rows live in physical pages of
+// 2^log2p >= 16 tokens of a [n_pages, Hkv, page, d] cache, so a 4-row chunk never straddles two
+// pages. Here wave w moves the consecutive chunks w * CPW .. w * CPW + CPW - 1, so it looks up a
+// physical page and builds a buffer resource only where its rows enter a new page (once or twice
+// per block); the chunks inside a page are immediate offsets from it. Lane k of `tbl` holds the
+// physical page of the block's k-th page-sized segment (segment 0 when a page holds the block).
+// Addressing stays 64-bit for caches of any size.
+template <int BLOCK, int NW, bool IS_K>
+__device__ __forceinline__ void copy_page_paged(const uint16_t* cache, long long page_elems,
+                                                int tbl, int first_row, int log2p, char* dst,
+                                                int w, int lane) {
+  constexpr int kChunks = BLOCK * kHeadDim * 2 / 1024;
+  constexpr int CPW = kChunks / NW;
+  static_assert(kChunks % NW == 0 && CPW % 4 == 0, "each wave moves a multiple of 16 rows");
+  const int page_mask = (1 << log2p) - 1;
+  // Opaque wave index: the per-chunk offsets are formed here instead of being hoisted out of the
+  // page loop into scalar registers.
+  asm volatile("" : "+s"(w));
+  __amdgpu_buffer_rsrc_t rs;
+  int u0 = 0;
+#pragma unroll
+  for (int u = 0; u < CPW; ++u) {
+    const int row_in_block = (w * CPW + u) * 4;
+    const int in_page = (first_row + row_in_block) & page_mask;
+    if (u == 0 || in_page == 0) {  // the wave's rows enter a (new) physical page
+      const long long phys = __builtin_amdgcn_readlane(tbl, row_in_block >> log2p);
+      const uint16_t* base = cache + phys * page_elems + (long long)in_page * kHeadDim;
+      rs = __builtin_amdgcn_make_buffer_rsrc((void*)base, (short)0,
+                                             ((page_mask + 1) - in_page) * kHeadDim * 2,
+                                             0x00020000);
+      u0 = u;
+    }
+    const int row = 4 * (w * CPW + u) + (lane >> 4);
+    const int stored = lane & 15;
+    const int slot = IS_K ? (stored ^ (row & 15)) : (stored ^ ((row & 3) << 2));
+    const int voff = (lane >> 4) * (kHeadDim * 2) + slot * 16;
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, COSA_LDS(dst + (w * CPW + u) * 1024), 16, voff,
+                                             (u - u0) * 1024, 0, 0);
+  }
+}
+
+template <int BLOCK, int HPW, bool OSK, bool PAGED>
 __global__ __attribute__((amdgpu_flat_work_group_size(TileCfg<BLOCK, HPW>::kThreads,
                                                       TileCfg<BLOCK, HPW>::kThreads)))
 __attribute__((amdgpu_waves_per_eu(TileCfg<BLOCK, HPW>::kWavesPerEu,
@@ -142,13 +186,55 @@ void attention_kernel(const AttnParams P) {
   };
   auto page_of = [&](int raw) -> int { return (unsigned)raw <= (unsigned)i ? raw : i; };
 
+  // Physical pages of a listed block (paged caches): lane k loads the page of the block's k-th
+  // page-sized segment; entries outside [0, n_pages) read page 0.
+  const int log2p = PAGED ? P.a.pg.log2_page : 0;
+  auto table_of = [&](int raw) -> int {
+    if constexpr (PAGED) {
+      const int segs = BLOCK >> log2p;
+      if (lane < (segs > 0 ? segs : 1)) {
+        const int lp = ((page_of(raw) * BLOCK) >> log2p) + lane;
+        const int e = P.a.pg.table[(size_t)n * P.a.pg.pages_per_seq + lp];
+        return (e >= 0 && (long long)e < P.a.pg.n_pages) ? e : 0;
+      }
+    }
+    return 0;
+  };
+  auto copy_block = [&](auto is_k, auto nwc, int raw, int tbl, char* dst, int wv)
+      __attribute__((always_inline)) {
+    constexpr bool IS_K = decltype(is_k)::value;
+    constexpr int NW = decltype(nwc)::value;
+    if constexpr (PAGED) {
+      // K or V cache of KV head g; one physical page of one head is page * d elements, pages of
+      // consecutive page numbers are Hkv of those apart
+      const long long head_page = (long long)kHeadDim << log2p;
+      const uint16_t* cache = (IS_K ? P.a.k : P.a.v) + (long long)g * head_page;
+      copy_page_paged<BLOCK, NW, IS_K>(cache, head_page * P.Hkv, tbl, page_of(raw) * BLOCK, log2p,
+                                       dst, wv, lane);
+    } else {
+      copy_page<BLOCK, NW, IS_K>(IS_K ? krs : vrs, dst, page_of(raw) * PAGE, wv, lane);
+    }
+  };
+
   // Prologue: K and V of page 0.
   const int raw0 = __builtin_amdgcn_readfirstlane(raw_entry(0));
   const int raw1 = __builtin_amdgcn_readfirstlane(raw_entry(1));
-  const int raw2 = raw_entry(2);
-  if (cnt > 0) {
-    copy_page<BLOCK, Cfg::kWaves, true>(krs, k_lds0, page_of(raw0) * PAGE, w, lane);
-    copy_page<BLOCK, Cfg::kWaves, false>(vrs, v_lds0, page_of(raw0) * PAGE, w, lane);
+  const int raw2 = __builtin_amdgcn_readfirstlane(raw_entry(2));
+  int tbl_nxt = 0;
+  if constexpr (PAGED) {
+    const int tbl0 = table_of(raw0);
+    tbl_nxt = table_of(raw1);
+    __builtin_amdgcn_s_waitcnt(kVmcntLgkm0);
+    if (cnt > 0) {
+      copy_block(std::true_type{}, std::integral_constant<int, Cfg::kWaves>{}, raw0, tbl0, k_lds0, w);
+      copy_block(std::false_type{}, std::integral_constant<int, Cfg::kWaves>{}, raw0, tbl0, v_lds0,
+                 w);
+    }
+  } else {
+    if (cnt > 0) {
+      copy_block(std::true_type{}, std::integral_constant<int, Cfg::kWaves>{}, raw0, 0, k_lds0, w);
+      copy_block(std::false_type{}, std::integral_constant<int, Cfg::kWaves>{}, raw0, 0, v_lds0, w);
+    }
   }
 
   // Q^T as the MFMA B operand: lane owns query row qrow, 8 chunks of 16 d (8 per lane half).
@@ -184,9 +270,10 @@ void attention_kernel(const AttnParams P) {
   }
   const size_t log_off = ((size_t)(n * P.Hq + h) * P.nb + i) * P.nb;
   int ncomp = 0;
-  // List entries of the phase's page m (cur) and m+1 (nxt), scalar; pre holds entry m+2 in flight.
-  int cur = raw0, nxt = raw1;
-  int pre = raw2;
+  // List entries of pages m (cur), m+1 (nxt) and m+2 (nxt2), scalar; pre holds entry m+3 in flight
+  // and, for paged caches, tbl_nxt2 the physical pages of entry m+2.
+  int cur = raw0, nxt = raw1, nxt2 = raw2;
+  int pre = 0, tbl_nxt2 = 0;
 
   __builtin_amdgcn_s_waitcnt(0);  // prologue pages, list entries and Q fragments
   __syncthreads();
@@ -333,16 +420,17 @@ void attention_kernel(const AttnParams P) {
   // Page kk, its buffers BUF: fetch page kk+1 into the other buffers, QK, barrier, PV, barrier.
   auto page = [&](int kk, auto bufc) __attribute__((always_inline)) {
     constexpr int BUF = decltype(bufc)::value;
-    pre = raw_entry(kk + 2);
+    pre = raw_entry(kk + 3);
+    if constexpr (PAGED) tbl_nxt2 = table_of(nxt2);
     if (kk + 1 < cnt) {
-      const int off = page_of(nxt) * PAGE;
+      constexpr auto NWH = std::integral_constant<int, WPH>{};
       if constexpr (HPW == 1) {
-        copy_page<BLOCK, WPH, true>(krs, BUF ? k_lds0 : k_lds1, off, wl, lane);
-        copy_page<BLOCK, WPH, false>(vrs, BUF ? v_lds0 : v_lds1, off, wl, lane);
+        copy_block(std::true_type{}, NWH, nxt, tbl_nxt, BUF ? k_lds0 : k_lds1, wl);
+        copy_block(std::false_type{}, NWH, nxt, tbl_nxt, BUF ? v_lds0 : v_lds1, wl);
       } else if (hw == 0) {
-        copy_page<BLOCK, WPH, true>(krs, BUF ? k_lds0 : k_lds1, off, wl, lane);
+        copy_block(std::true_type{}, NWH, nxt, tbl_nxt, BUF ? k_lds0 : k_lds1, wl);
       } else {
-        copy_page<BLOCK, WPH, false>(vrs, BUF ? v_lds0 : v_lds1, off, wl, lane);
+        copy_block(std::false_type{}, NWH, nxt, tbl_nxt, BUF ? v_lds0 : v_lds1, wl);
       }
     }
     qk_half(bufc);
@@ -350,7 +438,9 @@ void attention_kernel(const AttnParams P) {
     pv_half(kk, bufc);
     end_phase(true);
     cur = nxt;
-    nxt = __builtin_amdgcn_readfirstlane(pre);
+    nxt = nxt2;
+    nxt2 = __builtin_amdgcn_readfirstlane(pre);
+    tbl_nxt = tbl_nxt2;
   };
 
   if (HPW == 2 && hw == 1) end_phase(false);  // head slot 1 runs one phase behind
@@ -384,12 +474,24 @@ void attention_kernel(const AttnParams P) {
   }
 }
 
-template <int BLOCK, int HPW, bool OSK>
+template <int BLOCK, int HPW, bool OSK, bool PAGED>
 void launch_t(const AttnParams& P, int G, hipStream_t stream) {
   using Cfg = TileCfg<BLOCK, HPW>;
   const int slots = (P.n_units + kNumXcd - 1) / kNumXcd * kNumXcd * (G / HPW);
-  hipLaunchKernelGGL((attention_kernel<BLOCK, HPW, OSK>), dim3(slots), dim3(Cfg::kThreads), 0,
-                     stream, P);
+  hipLaunchKernelGGL((attention_kernel<BLOCK, HPW, OSK, PAGED>), dim3(slots), dim3(Cfg::kThreads),
+                     0, stream, P);
+}
+
+template <bool OSK, bool PAGED>
+void launch_shape(const Shape& sh, const AttnParams& P, hipStream_t stream) {
+  const bool pair = (sh.G % 2) == 0;
+  if (sh.b == 128) {
+    if (pair) launch_t<128, 2, OSK, PAGED>(P, sh.G, stream);
+    else launch_t<128, 1, OSK, PAGED>(P, sh.G, stream);
+  } else {
+    if (pair) launch_t<64, 2, OSK, PAGED>(P, sh.G, stream);
+    else launch_t<64, 1, OSK, PAGED>(P, sh.G, stream);
+  }
 }
 
 template <bool OSK>
@@ -404,13 +506,11 @@ hipError_t launch(const Shape& sh, const AttnArgs& a, hipStream_t stream) {
   P.n_units = sh.B * sh.Hkv * sh.nb;
   P.scale = sh.scale;
   P.scale_log2 = sh.scale * 1.4426950408889634f;
-  const bool pair = (sh.G % 2) == 0;
-  if (sh.b == 128) {
-    if (pair) launch_t<128, 2, OSK>(P, sh.G, stream);
-    else launch_t<128, 1, OSK>(P, sh.G, stream);
+  if constexpr (OSK) {
+    if (a.pg.table != nullptr) launch_shape<true, true>(sh, P, stream);
+    else launch_shape<true, false>(sh, P, stream);
   } else {
-    if (pair) launch_t<64, 2, OSK>(P, sh.G, stream);
-    else launch_t<64, 1, OSK>(P, sh.G, stream);
+    launch_shape<false, false>(sh, P, stream);
   }
   return hipGetLastError();
 }

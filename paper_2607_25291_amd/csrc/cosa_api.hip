@@ -120,6 +120,31 @@ cosa_status check_skip(const cosa_skip* sk, const cosa::Shape& sh, int& on, floa
   return ok();
 }
 
+// Validates a paged KV cache description against the problem and fills the internal form.
+cosa_status check_paged(const cosa_paged_kv* kv, const cosa::Shape& sh, bool need_v,
+                        cosa::KvPages& pg) {
+  if (!kv) return fail(COSA_ERR_INVALID_ARG, "paged kv is NULL");
+  const int ps = kv->page_size;
+  if (ps < 16 || ps > (1 << 20) || (ps & (ps - 1)) != 0)
+    return fail(COSA_ERR_INVALID_ARG, "page_size %d is not a power of two in [16, 2^20]", ps);
+  if (sh.L % ps != 0)
+    return fail(COSA_ERR_INVALID_ARG, "page_size %d does not divide seq_len %d", ps, sh.L);
+  if (kv->n_pages < 1) return fail(COSA_ERR_INVALID_ARG, "n_pages (%lld) must be >= 1",
+                                   (long long)kv->n_pages);
+  if (kv->n_pages > (1LL << 31))
+    return fail(COSA_ERR_INVALID_ARG, "n_pages (%lld) exceeds the int32 page numbers of the table",
+                (long long)kv->n_pages);
+  if (!kv->k_cache || !kv->page_table || (need_v && !kv->v_cache))
+    return fail(COSA_ERR_INVALID_ARG, "k_cache%s and page_table must be non-NULL",
+                need_v ? ", v_cache" : "");
+  pg.table = kv->page_table;
+  pg.log2_page = 0;
+  while ((1 << pg.log2_page) < ps) ++pg.log2_page;
+  pg.pages_per_seq = sh.L / ps;
+  pg.n_pages = kv->n_pages;
+  return ok();
+}
+
 size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 
 cosa_workspace_layout layout_of(const cosa::Shape& sh) {
@@ -135,6 +160,50 @@ cosa_workspace_layout layout_of(const cosa::Shape& sh) {
 }
 
 hipStream_t as_stream(void* s) { return reinterpret_cast<hipStream_t>(s); }
+
+// Algorithm A end to end; kv == nullptr: contiguous K and V at k, v.
+cosa_status prefill(const cosa_problem* problem, const void* q, const void* k, const void* v,
+                    const cosa_paged_kv* kv, const cosa_select* select, const cosa_skip* skip,
+                    void* workspace, size_t workspace_bytes, void* o, void* stream) {
+  cosa::Shape sh;
+  bool empty = false;
+  cosa_status st = make_shape(problem, sh, empty);
+  if (st != COSA_OK) return st;
+  int64_t micro = 0;
+  if ((st = check_select(select, micro)) != COSA_OK) return st;
+  int on = 0;
+  float tau = 0.f;
+  if ((st = check_skip(skip, sh, on, tau)) != COSA_OK) return st;
+  cosa::KvPages pg{};
+  if (kv && (st = check_paged(kv, sh, true, pg)) != COSA_OK) return st;
+  if (empty) return ok();
+  if ((st = check_proxy_limits(sh)) != COSA_OK) return st;
+  if (!q || !k || !v || !o) return fail(COSA_ERR_INVALID_ARG, "q, k, v and o must be non-NULL");
+  const cosa_workspace_layout l = layout_of(sh);
+  if (!workspace || workspace_bytes < l.total)
+    return fail(COSA_ERR_WORKSPACE, "workspace of %zu bytes at %p, need %zu", workspace_bytes,
+                workspace, l.total);
+  char* ws = static_cast<char*>(workspace);
+  float* score = reinterpret_cast<float*>(ws + l.score);
+  uint8_t* hrm = reinterpret_cast<uint8_t*>(ws + l.hrm);
+  int32_t* order = reinterpret_cast<int32_t*>(ws + l.order);
+  int32_t* count = reinterpret_cast<int32_t*>(ws + l.count);
+  const hipStream_t s = as_stream(stream);
+  hipError_t e = cosa::launch_kap_score(
+      sh, cosa::KapScoreArgs{static_cast<const uint16_t*>(q), static_cast<const uint16_t*>(k), score,
+                             hrm, pg},
+      s);
+  if (e != hipSuccess) return hip_fail(e, "kap_score launch");
+  e = cosa::launch_kap_select(
+      sh, cosa::KapSelectArgs{score, hrm, order, count, (int)select->mode, (int)select->order, micro},
+      s);
+  if (e != hipSuccess) return hip_fail(e, "kap_select launch");
+  cosa::AttnArgs a{static_cast<const uint16_t*>(q), static_cast<const uint16_t*>(k),
+                   static_cast<const uint16_t*>(v), static_cast<uint16_t*>(o), order, count,
+                   nullptr, nullptr, nullptr, on, tau, pg};
+  e = cosa::launch_osk_attention(sh, a, s);
+  return e == hipSuccess ? ok() : hip_fail(e, "osk_attention launch");
+}
 
 }  // namespace
 
@@ -163,7 +232,26 @@ cosa_status cosa_kap_score(const cosa_problem* problem, const void* q, const voi
   if ((st = check_proxy_limits(sh)) != COSA_OK) return st;
   if (!q || !k || !score || !hrm)
     return fail(COSA_ERR_INVALID_ARG, "q, k, score and hrm must be non-NULL");
-  cosa::KapScoreArgs a{static_cast<const uint16_t*>(q), static_cast<const uint16_t*>(k), score, hrm};
+  cosa::KapScoreArgs a{static_cast<const uint16_t*>(q), static_cast<const uint16_t*>(k), score, hrm,
+                       cosa::KvPages{}};
+  const hipError_t e = cosa::launch_kap_score(sh, a, as_stream(stream));
+  return e == hipSuccess ? ok() : hip_fail(e, "kap_score launch");
+}
+
+cosa_status cosa_kap_score_paged(const cosa_problem* problem, const void* q,
+                                 const cosa_paged_kv* kv, float* score, uint8_t* hrm,
+                                 void* stream) {
+  cosa::Shape sh;
+  bool empty = false;
+  cosa_status st = make_shape(problem, sh, empty);
+  if (st != COSA_OK) return st;
+  cosa::KvPages pg{};
+  if ((st = check_paged(kv, sh, false, pg)) != COSA_OK) return st;
+  if (empty) return ok();
+  if ((st = check_proxy_limits(sh)) != COSA_OK) return st;
+  if (!q || !score || !hrm) return fail(COSA_ERR_INVALID_ARG, "q, score and hrm must be non-NULL");
+  cosa::KapScoreArgs a{static_cast<const uint16_t*>(q), static_cast<const uint16_t*>(kv->k_cache),
+                       score, hrm, pg};
   const hipError_t e = cosa::launch_kap_score(sh, a, as_stream(stream));
   return e == hipSuccess ? ok() : hip_fail(e, "kap_score launch");
 }
@@ -201,7 +289,31 @@ cosa_status cosa_osk_attention(const cosa_problem* problem, const void* q, const
     return fail(COSA_ERR_INVALID_ARG, "q, k, v, order, count and o must be non-NULL");
   cosa::AttnArgs a{static_cast<const uint16_t*>(q), static_cast<const uint16_t*>(k),
                    static_cast<const uint16_t*>(v), static_cast<uint16_t*>(o), order, count,
-                   visit_log, margin_log, n_computed, on, tau};
+                   visit_log, margin_log, n_computed, on, tau, cosa::KvPages{}};
+  const hipError_t e = cosa::launch_osk_attention(sh, a, as_stream(stream));
+  return e == hipSuccess ? ok() : hip_fail(e, "osk_attention launch");
+}
+
+cosa_status cosa_osk_attention_paged(const cosa_problem* problem, const void* q,
+                                     const cosa_paged_kv* kv, const int32_t* order,
+                                     const int32_t* count, const cosa_skip* skip, void* o,
+                                     uint8_t* visit_log, float* margin_log, int32_t* n_computed,
+                                     void* stream) {
+  cosa::Shape sh;
+  bool empty = false;
+  cosa_status st = make_shape(problem, sh, empty);
+  if (st != COSA_OK) return st;
+  int on = 0;
+  float tau = 0.f;
+  if ((st = check_skip(skip, sh, on, tau)) != COSA_OK) return st;
+  cosa::KvPages pg{};
+  if ((st = check_paged(kv, sh, true, pg)) != COSA_OK) return st;
+  if (empty) return ok();
+  if (!q || !order || !count || !o)
+    return fail(COSA_ERR_INVALID_ARG, "q, order, count and o must be non-NULL");
+  cosa::AttnArgs a{static_cast<const uint16_t*>(q), static_cast<const uint16_t*>(kv->k_cache),
+                   static_cast<const uint16_t*>(kv->v_cache), static_cast<uint16_t*>(o), order,
+                   count, visit_log, margin_log, n_computed, on, tau, pg};
   const hipError_t e = cosa::launch_osk_attention(sh, a, as_stream(stream));
   return e == hipSuccess ? ok() : hip_fail(e, "osk_attention launch");
 }
@@ -216,7 +328,7 @@ cosa_status cosa_dense_attention(const cosa_problem* problem, const void* q, con
   if (!q || !k || !v || !o) return fail(COSA_ERR_INVALID_ARG, "q, k, v and o must be non-NULL");
   cosa::AttnArgs a{static_cast<const uint16_t*>(q), static_cast<const uint16_t*>(k),
                    static_cast<const uint16_t*>(v), static_cast<uint16_t*>(o), nullptr, nullptr,
-                   nullptr, nullptr, nullptr, 0, 0.f};
+                   nullptr, nullptr, nullptr, 0, 0.f, cosa::KvPages{}};
   const hipError_t e = cosa::launch_dense_attention(sh, a, as_stream(stream));
   return e == hipSuccess ? ok() : hip_fail(e, "dense_attention launch");
 }
@@ -241,42 +353,15 @@ size_t cosa_prefill_workspace_bytes(const cosa_problem* problem) {
 cosa_status cosa_prefill(const cosa_problem* problem, const void* q, const void* k, const void* v,
                          const cosa_select* select, const cosa_skip* skip, void* workspace,
                          size_t workspace_bytes, void* o, void* stream) {
-  cosa::Shape sh;
-  bool empty = false;
-  cosa_status st = make_shape(problem, sh, empty);
-  if (st != COSA_OK) return st;
-  int64_t micro = 0;
-  if ((st = check_select(select, micro)) != COSA_OK) return st;
-  int on = 0;
-  float tau = 0.f;
-  if ((st = check_skip(skip, sh, on, tau)) != COSA_OK) return st;
-  if (empty) return ok();
-  if ((st = check_proxy_limits(sh)) != COSA_OK) return st;
-  if (!q || !k || !v || !o) return fail(COSA_ERR_INVALID_ARG, "q, k, v and o must be non-NULL");
-  const cosa_workspace_layout l = layout_of(sh);
-  if (!workspace || workspace_bytes < l.total)
-    return fail(COSA_ERR_WORKSPACE, "workspace of %zu bytes at %p, need %zu", workspace_bytes,
-                workspace, l.total);
-  char* ws = static_cast<char*>(workspace);
-  float* score = reinterpret_cast<float*>(ws + l.score);
-  uint8_t* hrm = reinterpret_cast<uint8_t*>(ws + l.hrm);
-  int32_t* order = reinterpret_cast<int32_t*>(ws + l.order);
-  int32_t* count = reinterpret_cast<int32_t*>(ws + l.count);
-  const hipStream_t s = as_stream(stream);
-  hipError_t e = cosa::launch_kap_score(
-      sh, cosa::KapScoreArgs{static_cast<const uint16_t*>(q), static_cast<const uint16_t*>(k), score,
-                             hrm},
-      s);
-  if (e != hipSuccess) return hip_fail(e, "kap_score launch");
-  e = cosa::launch_kap_select(
-      sh, cosa::KapSelectArgs{score, hrm, order, count, (int)select->mode, (int)select->order, micro},
-      s);
-  if (e != hipSuccess) return hip_fail(e, "kap_select launch");
-  cosa::AttnArgs a{static_cast<const uint16_t*>(q), static_cast<const uint16_t*>(k),
-                   static_cast<const uint16_t*>(v), static_cast<uint16_t*>(o), order, count,
-                   nullptr, nullptr, nullptr, on, tau};
-  e = cosa::launch_osk_attention(sh, a, s);
-  return e == hipSuccess ? ok() : hip_fail(e, "osk_attention launch");
+  return prefill(problem, q, k, v, nullptr, select, skip, workspace, workspace_bytes, o, stream);
+}
+
+cosa_status cosa_prefill_paged(const cosa_problem* problem, const void* q, const cosa_paged_kv* kv,
+                               const cosa_select* select, const cosa_skip* skip, void* workspace,
+                               size_t workspace_bytes, void* o, void* stream) {
+  if (!kv) return fail(COSA_ERR_INVALID_ARG, "paged kv is NULL");
+  return prefill(problem, q, kv->k_cache, kv->v_cache, kv, select, skip, workspace,
+                 workspace_bytes, o, stream);
 }
 
 }  // extern "C"

@@ -17,11 +17,22 @@ struct Shape {
   float scale;  // resolved sm_scale
 };
 
+// Where a KV head's keys and values live. table == nullptr: contiguous [B, Hkv, L, d] at the K/V
+// pointers of the call. Otherwise a paged cache [n_pages, Hkv, page, d] per tensor and a page table
+// [B, L / page] of physical page numbers (entries are clamped into [0, n_pages) on the device).
+struct KvPages {
+  const int32_t* table;
+  int log2_page;       // page = 1 << log2_page tokens
+  int pages_per_seq;   // L / page
+  long long n_pages;
+};
+
 struct KapScoreArgs {
   const uint16_t* q;
-  const uint16_t* k;
+  const uint16_t* k;   // contiguous K, or the paged K cache
   float* score;
   uint8_t* hrm;
+  KvPages pg;
 };
 
 struct KapSelectArgs {
@@ -46,6 +57,7 @@ struct AttnArgs {
   int32_t* n_computed;    // optional
   int skip_on;
   float tau;              // skip threshold in nats (float32)
+  KvPages pg;             // k and v are the paged caches when pg.table != nullptr (OSK only)
 };
 
 // LDS bytes the proxy-scoring kernel needs for a shape (0 if the shape is outside its limits).

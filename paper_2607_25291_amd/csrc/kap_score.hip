@@ -27,7 +27,7 @@ struct KapParams {
   float scale;
 };
 
-template <int SPB, int RT>
+template <int SPB, int RT, bool PAGED>
 __global__ __launch_bounds__(kScoreThreads) void kap_score_kernel(const KapParams P) {
   extern __shared__ float beta[];  // [R][nbp]
   __shared__ float mu[RT * 32];
@@ -60,10 +60,24 @@ __global__ __launch_bounds__(kScoreThreads) void kap_score_kernel(const KapParam
   }
 
   const uint16_t* kbase = P.a.k + (size_t)ng * P.L * kHeadDim + 8 * half;
+  // Row of sampled key c (token c * s): contiguous K, or its physical page in a paged cache
+  // [n_pages, Hkv, page, d] through the page table (entries outside [0, n_pages) read page 0).
+  auto key_row = [&](int c) -> const uint16_t* {
+    if constexpr (PAGED) {
+      const int t = c * P.s;
+      const int log2p = P.a.pg.log2_page;
+      int e = P.a.pg.table[(size_t)n * P.a.pg.pages_per_seq + (t >> log2p)];
+      e = (e >= 0 && (long long)e < P.a.pg.n_pages) ? e : 0;
+      const long long row = (((long long)e * P.Hkv + g) << log2p) + (t & ((1 << log2p) - 1));
+      return P.a.k + row * kHeadDim + 8 * half;
+    } else {
+      return kbase + (size_t)c * P.s * kHeadDim;
+    }
+  };
   auto load_keys = [&](int chunk, bf16x8_t (&kf)[8]) __attribute__((always_inline)) {
     const int c = chunk * 32 + l32;
     if (chunk < nchunks && c < nkeys) {
-      const uint16_t* kp = kbase + (size_t)c * P.s * kHeadDim;
+      const uint16_t* kp = key_row(c);
 #pragma unroll
       for (int cc = 0; cc < 8; ++cc) kf[cc] = as_bf16x8(ldg16(kp + 16 * cc));
     } else {
@@ -169,7 +183,7 @@ __global__ __launch_bounds__(kScoreThreads) void kap_score_kernel(const KapParam
   }
 }
 
-template <int SPB, int RT>
+template <int SPB, int RT, bool PAGED>
 hipError_t launch_t(const KapParams& P, size_t lds, hipStream_t stream) {
   // Dynamic LDS above the default limit has to be allowed per kernel; remember the largest size
   // granted so far for this instantiation.
@@ -179,23 +193,29 @@ hipError_t launch_t(const KapParams& P, size_t lds, hipStream_t stream) {
     std::lock_guard<std::mutex> lock(mu);
     if (lds > granted) {
       const hipError_t e =
-          hipFuncSetAttribute(reinterpret_cast<const void*>(&kap_score_kernel<SPB, RT>),
+          hipFuncSetAttribute(reinterpret_cast<const void*>(&kap_score_kernel<SPB, RT, PAGED>),
                               hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
       if (e != hipSuccess) return e;
       granted = lds;
     }
   }
-  hipLaunchKernelGGL((kap_score_kernel<SPB, RT>), dim3(P.n_units), dim3(kScoreThreads), lds,
+  hipLaunchKernelGGL((kap_score_kernel<SPB, RT, PAGED>), dim3(P.n_units), dim3(kScoreThreads), lds,
                      stream, P);
   return hipGetLastError();
 }
 
+template <int SPB, bool PAGED>
+hipError_t launch_rt(const KapParams& P, size_t lds, hipStream_t stream) {
+  const int rt = (P.R + 31) / 32;
+  if (rt <= 1) return launch_t<SPB, 1, PAGED>(P, lds, stream);
+  if (rt <= 2) return launch_t<SPB, 2, PAGED>(P, lds, stream);
+  return launch_t<SPB, 4, PAGED>(P, lds, stream);
+}
+
 template <int SPB>
 hipError_t launch_spb(const KapParams& P, size_t lds, hipStream_t stream) {
-  const int rt = (P.R + 31) / 32;
-  if (rt <= 1) return launch_t<SPB, 1>(P, lds, stream);
-  if (rt <= 2) return launch_t<SPB, 2>(P, lds, stream);
-  return launch_t<SPB, 4>(P, lds, stream);
+  if (P.a.pg.table != nullptr) return launch_rt<SPB, true>(P, lds, stream);
+  return launch_rt<SPB, false>(P, lds, stream);
 }
 
 }  // namespace

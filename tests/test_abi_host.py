@@ -13,7 +13,8 @@ from paper_2607_25291_amd.calibrate import delta_for_budget
 
 EXPECTED = {"cosa_status_string", "cosa_last_error", "cosa_kap_score", "cosa_kap_select_ordered",
             "cosa_osk_attention", "cosa_dense_attention", "cosa_prefill_workspace_bytes",
-            "cosa_prefill_workspace_layout", "cosa_prefill"}
+            "cosa_prefill_workspace_layout", "cosa_prefill", "cosa_kap_score_paged",
+            "cosa_osk_attention_paged", "cosa_prefill_paged"}
 
 
 def test_header_declares_the_abi():
@@ -98,6 +99,32 @@ def test_argument_validation():
         B.cosa_prefill(GOOD, 16, 16, 16, B.select(B.SELECT_FRACTION, 0.5), None, None, ws, 16,
                        stream=0)
     assert e.value.status == B.COSA_ERR_WORKSPACE
+
+
+def test_paged_validation():
+    def kv(page=64, n_pages=16, k=16, v=16, table=16):
+        return B.CosaPagedKv(k, v, table, page, n_pages)
+    sel = B.select(B.SELECT_FRACTION, 0.5)
+    ws = B.cosa_prefill_workspace_bytes(GOOD)
+    for bad in [kv(page=48), kv(page=8), kv(page=1 << 21), kv(page=2048), kv(n_pages=0),
+                kv(n_pages=2 ** 40), kv(table=None), kv(k=None), kv(v=None)]:
+        with pytest.raises(B.CosaError) as e:
+            B.cosa_osk_attention_paged(GOOD, 16, bad, 16, 16, None, 16, stream=0)
+        assert e.value.status == B.COSA_ERR_INVALID_ARG
+        with pytest.raises(B.CosaError) as e:
+            B.cosa_prefill_paged(GOOD, 16, bad, sel, None, 16, ws, 16, stream=0)
+        assert e.value.status == B.COSA_ERR_INVALID_ARG
+    for bad in [kv(page=48), kv(table=None), kv(k=None)]:
+        with pytest.raises(B.CosaError) as e:
+            B.cosa_kap_score_paged(GOOD, 16, bad, 16, 16, stream=0)
+        assert e.value.status == B.COSA_ERR_INVALID_ARG
+    with pytest.raises(B.CosaError) as e:
+        B.cosa_prefill_paged(GOOD, 16, None, sel, None, 16, ws, 16, stream=0)
+    assert e.value.status == B.COSA_ERR_INVALID_ARG
+    # the proxy alone does not need the V cache (an empty problem validates and launches nothing)
+    B.cosa_kap_score_paged(B.Problem(0, 8, 2, 1024), None, kv(v=None), None, None, stream=0)
+    B.cosa_prefill_paged(B.Problem(0, 8, 2, 1024), None, kv(), sel, None, None, 0, None, stream=0)
+    assert B.cosa_last_error() == ""
 
 
 def test_empty_problems_launch_nothing():
