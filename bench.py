@@ -2,6 +2,7 @@
 
     python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload qwen3_8b_l128k]
     python bench.py --sweep [--steps K]     # budget / visiting-order sweep (one JSON object)
+    python bench.py --microbench [--steps K]  # list walk vs mask walk vs dense (one JSON object)
 
 A step is one pass of the whole hot path, cosa_prefill (proxy scoring, ordered selection, ordered-
 skipping attention) over one attention layer of synthetic bf16 inputs that are already resident in
@@ -219,6 +220,77 @@ def run_sweep(args):
                       "records": recs}), flush=True)
 
 
+def run_microbench(args):
+    """Kernel microbenchmark (appendix D "Kernel microbenchmark"): at matched budgets
+    B in {25, 50, 75} % and L in {32K, 64K, 128K} (32 query / 8 KV heads, d = 128, b = 128), the
+    OSK's index-driven walk over the selected blocks (KAP order, and the same set ascending) against
+    the in-loop logical skipping of a block mask over every causal block, and the dense kernel.
+    Skipping is off, so every variant computes exactly the selected set. One JSON object.
+    """
+    import dataclasses
+
+    import torch
+    from paper_2607_25291_amd import binding as B
+    from paper_2607_25291_amd.inputs import WORKLOADS, make_inputs
+
+    dev = torch.device("cuda:0")
+    base = WORKLOADS["qwen3_8b_l128k"]
+
+    def timeit(fn, n):
+        fn()
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(n):
+            fn()
+        e1.record()
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) / n
+
+    recs = []
+    for L in (32768, 65536, 131072):
+        w = dataclasses.replace(base, name=f"qwen3_8b_l{L // 1024}k", seq_len=L)
+        nb = w.n_blocks
+        log(f"[microbench] L={L}: generating inputs")
+        q_np, k_np, v_np = make_inputs(w)
+        up = lambda a: torch.from_numpy(a.view(np.int16)).to(dev)
+        q, k, v = up(q_np), up(k_np), up(v_np)
+        p = B.Problem(w.batch, w.n_q_heads, w.n_kv_heads, L, w.head_dim, w.block, w.stride)
+        o = torch.empty_like(q)
+        shp = (w.batch, w.n_kv_heads, nb, nb)
+        score = torch.zeros(shp, dtype=torch.float32, device=dev)
+        hrm = torch.zeros(shp, dtype=torch.uint8, device=dev)
+        order = torch.zeros(shp, dtype=torch.int32, device=dev)
+        count = torch.zeros(shp[:3], dtype=torch.int32, device=dev)
+        t_dense = timeit(lambda: B.cosa_dense_attention(p, q, k, v, o), max(1, args.steps // 2))
+        log(f"[microbench] L={L} dense {t_dense:.3f} ms")
+        B.cosa_kap_score(p, q, k, score, hrm)
+        for budget in (0.25, 0.50, 0.75):
+            row = {"seq_len": L, "budget": budget, "dense_ms": round(t_dense, 3)}
+            for mode, key in ((B.ORDER_KAP, "osk_kap_order_ms"),
+                              (B.ORDER_ASCENDING, "osk_ascending_ms")):
+                B.cosa_kap_select_ordered(p, score, hrm, B.select(B.SELECT_FRACTION, budget, mode),
+                                          order, count)
+                row[key] = round(timeit(lambda: B.cosa_osk_attention(
+                    p, q, k, v, order, count, None, o), args.steps), 3)
+            # the same set as a block mask, walked with in-loop (logical) skipping
+            mask = torch.zeros(shp, dtype=torch.uint8, device=dev)
+            valid = (torch.arange(nb, device=dev).view(1, 1, 1, nb) < count.unsqueeze(-1))
+            mask.scatter_add_(-1, order.clamp(min=0).long(), valid.to(torch.uint8))
+            row["masked_ms"] = round(timeit(lambda: B.cosa_masked_attention(
+                p, q, k, v, mask, o), args.steps), 3)
+            causal = w.batch * w.n_kv_heads * nb * (nb + 1) // 2
+            row["realized_budget"] = round(int(count.sum()) / causal, 5)
+            for key in ("osk_kap_order_ms", "osk_ascending_ms", "masked_ms"):
+                row[key.replace("_ms", "_speedup")] = round(t_dense / row[key], 3)
+            log(f"[microbench] {row}")
+            recs.append(row)
+            del mask
+        del q, k, v, o, score, hrm, order, count
+        torch.cuda.empty_cache()
+    print(json.dumps({"steps": args.steps, "data": "synthetic", "records": recs}), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -230,6 +302,9 @@ def main():
     ap.add_argument("--page-size", type=int, default=0,
                     help="time cosa_prefill_paged on a paged KV cache with this page size "
                          "(pages placed by a random permutation); 0: contiguous K/V")
+    ap.add_argument("--microbench", action="store_true",
+                    help="kernel microbenchmark: OSK list walk vs mask walk vs dense over "
+                         "B in {25, 50, 75}% and L in {32K, 64K, 128K}")
     ap.add_argument("--sweep", action="store_true",
                     help="run the budget / visiting-order sweep instead of the one-line benchmark")
     ap.add_argument("--copy-probe-mib", type=int, default=0,
@@ -242,6 +317,9 @@ def main():
         sys.exit(2)
     if args.sweep:
         run_sweep(args)
+        return
+    if args.microbench:
+        run_microbench(args)
         return
 
     import torch

@@ -188,6 +188,19 @@ cosa_status cosa_osk_attention(const cosa_problem* problem, const void* q, const
 cosa_status cosa_dense_attention(const cosa_problem* problem, const void* q, const void* k,
                                  const void* v, void* o, void* stream);
 
+/*
+ * Block-sparse attention under a binary block mask with logical skipping (Sec. 3.2, Eq.
+ * (proxy-mask); the mask-driven scheme the OSK is compared with in appendix D "Kernel
+ * microbenchmark"). Query head h of batch n and query block i visits j = 0 .. i in ascending order
+ * and computes block j exactly when mask[n, g(h), i, j] != 0 (u8 [B, Hkv, nb, nb]; entries j > i
+ * are not read). A masked block costs a step of the walk but no loads and no arithmetic. Same tile
+ * code and numerics as cosa_osk_attention; on the same block set the output equals
+ * cosa_osk_attention over the ascending list without skipping, bit for bit. A row with no block
+ * selected yields O = 0.
+ */
+cosa_status cosa_masked_attention(const cosa_problem* problem, const void* q, const void* k,
+                                  const void* v, const uint8_t* mask, void* o, void* stream);
+
 /* Workspace size of cosa_prefill (0 if the problem is invalid; see cosa_last_error()). */
 size_t cosa_prefill_workspace_bytes(const cosa_problem* problem);
 

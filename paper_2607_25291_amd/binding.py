@@ -116,6 +116,8 @@ def lib():
         L.cosa_prefill.restype = S
         L.cosa_prefill.argtypes = [P, vp, vp, vp, ctypes.POINTER(CosaSelect),
                                    ctypes.POINTER(CosaSkip), vp, ctypes.c_size_t, vp, vp]
+        L.cosa_masked_attention.restype = S
+        L.cosa_masked_attention.argtypes = [P, vp, vp, vp, vp, vp, vp]
         KV = ctypes.POINTER(CosaPagedKv)
         L.cosa_kap_score_paged.restype = S
         L.cosa_kap_score_paged.argtypes = [P, vp, KV, vp, vp, vp]
@@ -201,6 +203,12 @@ def cosa_dense_attention(problem, q, k, v, o, stream=None):
     p = _prob(problem)
     _check(lib().cosa_dense_attention(ctypes.byref(p), _ptr(q), _ptr(k), _ptr(v), _ptr(o),
                                       _stream(stream)))
+
+
+def cosa_masked_attention(problem, q, k, v, mask, o, stream=None):
+    p = _prob(problem)
+    _check(lib().cosa_masked_attention(ctypes.byref(p), _ptr(q), _ptr(k), _ptr(v), _ptr(mask),
+                                       _ptr(o), _stream(stream)))
 
 
 def cosa_prefill_workspace_bytes(problem) -> int:

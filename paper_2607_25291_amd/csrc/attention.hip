@@ -132,13 +132,20 @@ __device__ __forceinline__ void copy_page_paged(const uint16_t* cache, long long
   }
 }
 
-template <int BLOCK, int HPW, bool OSK, bool PAGED>
+// How the key blocks of a query block are walked.
+constexpr int kWalkDense = 0;  // j = 0 .. i ascending, every block computed
+constexpr int kWalkList = 1;   // OSK: the KAP list in list order, rowmax skip vote
+constexpr int kWalkMask = 2;   // j = 0 .. i ascending, blocks whose mask byte is 0 skipped in-loop
+
+template <int BLOCK, int HPW, int WALK, bool PAGED>
 __global__ __attribute__((amdgpu_flat_work_group_size(TileCfg<BLOCK, HPW>::kThreads,
                                                       TileCfg<BLOCK, HPW>::kThreads)))
 __attribute__((amdgpu_waves_per_eu(TileCfg<BLOCK, HPW>::kWavesPerEu,
                                    TileCfg<BLOCK, HPW>::kWavesPerEu)))
 void attention_kernel(const AttnParams P) {
   using Cfg = TileCfg<BLOCK, HPW>;
+  constexpr bool OSK = WALK == kWalkList;
+  constexpr bool MASKED = WALK == kWalkMask;
   constexpr int KT = Cfg::kKeyTiles;
   constexpr int WPH = Cfg::kWavesPerHead;
   constexpr int PAGE = Cfg::kPage;
@@ -171,19 +178,24 @@ void attention_kernel(const AttnParams P) {
 
   int cnt;
   const int32_t* lst = nullptr;
+  const uint8_t* mrow = nullptr;
   if constexpr (OSK) {
     cnt = P.a.count[(size_t)ng * P.nb + i];
     cnt = cnt < P.nb ? cnt : P.nb;
     lst = P.a.order + ((size_t)ng * P.nb + i) * P.nb;
   } else {
     cnt = i + 1;
+    if constexpr (MASKED) mrow = P.a.mask + ((size_t)ng * P.nb + i) * P.nb;
   }
   // List entries, read ahead of their use. A malformed entry (outside [0, i]) is fetched as block
-  // i but contributes nothing.
+  // i but contributes nothing. With a block mask, a masked block's entry is -1: nothing is fetched
+  // or computed for it, but the walk still steps through it (logical skipping).
   auto raw_entry = [&](int kk) -> int {
     if constexpr (OSK) return kk < cnt ? lst[kk] : 0;
+    else if constexpr (MASKED) return (kk < cnt && mrow[kk] != 0) ? kk : -1;
     else return kk;
   };
+  auto listed = [&](int raw) -> bool { return (unsigned)raw <= (unsigned)i; };
   auto page_of = [&](int raw) -> int { return (unsigned)raw <= (unsigned)i ? raw : i; };
 
   // Physical pages of a listed block (paged caches): lane k loads the page of the block's k-th
@@ -231,7 +243,7 @@ void attention_kernel(const AttnParams P) {
                  w);
     }
   } else {
-    if (cnt > 0) {
+    if (cnt > 0 && (!MASKED || listed(raw0))) {
       copy_block(std::true_type{}, std::integral_constant<int, Cfg::kWaves>{}, raw0, 0, k_lds0, w);
       copy_block(std::false_type{}, std::integral_constant<int, Cfg::kWaves>{}, raw0, 0, v_lds0, w);
     }
@@ -288,7 +300,8 @@ void attention_kernel(const AttnParams P) {
     constexpr int BUF = decltype(bufc)::value;
     const char* Kb = BUF ? k_lds1 : k_lds0;
     const int j = page_of(cur);
-    v_pend = OSK ? ((unsigned)cur <= (unsigned)i) : true;
+    v_pend = (OSK || MASKED) ? listed(cur) : true;
+    if (MASKED && !v_pend) return;  // a masked block: no Q K^T either
     // S^T tile t: keys 32 t + 8 (r / 4) + 4 half + r % 4 (register r) of query row qrow. The d chunk
     // is the outer loop: the KT tiles are independent accumulation chains, and each chunk's KT
     // fragments are read from LDS as one batch.
@@ -422,7 +435,7 @@ void attention_kernel(const AttnParams P) {
     constexpr int BUF = decltype(bufc)::value;
     pre = raw_entry(kk + 3);
     if constexpr (PAGED) tbl_nxt2 = table_of(nxt2);
-    if (kk + 1 < cnt) {
+    if (kk + 1 < cnt && (!MASKED || listed(nxt))) {
       constexpr auto NWH = std::integral_constant<int, WPH>{};
       if constexpr (HPW == 1) {
         copy_block(std::true_type{}, NWH, nxt, tbl_nxt, BUF ? k_lds0 : k_lds1, wl);
@@ -474,27 +487,27 @@ void attention_kernel(const AttnParams P) {
   }
 }
 
-template <int BLOCK, int HPW, bool OSK, bool PAGED>
+template <int BLOCK, int HPW, int WALK, bool PAGED>
 void launch_t(const AttnParams& P, int G, hipStream_t stream) {
   using Cfg = TileCfg<BLOCK, HPW>;
   const int slots = (P.n_units + kNumXcd - 1) / kNumXcd * kNumXcd * (G / HPW);
-  hipLaunchKernelGGL((attention_kernel<BLOCK, HPW, OSK, PAGED>), dim3(slots), dim3(Cfg::kThreads),
+  hipLaunchKernelGGL((attention_kernel<BLOCK, HPW, WALK, PAGED>), dim3(slots), dim3(Cfg::kThreads),
                      0, stream, P);
 }
 
-template <bool OSK, bool PAGED>
+template <int WALK, bool PAGED>
 void launch_shape(const Shape& sh, const AttnParams& P, hipStream_t stream) {
   const bool pair = (sh.G % 2) == 0;
   if (sh.b == 128) {
-    if (pair) launch_t<128, 2, OSK, PAGED>(P, sh.G, stream);
-    else launch_t<128, 1, OSK, PAGED>(P, sh.G, stream);
+    if (pair) launch_t<128, 2, WALK, PAGED>(P, sh.G, stream);
+    else launch_t<128, 1, WALK, PAGED>(P, sh.G, stream);
   } else {
-    if (pair) launch_t<64, 2, OSK, PAGED>(P, sh.G, stream);
-    else launch_t<64, 1, OSK, PAGED>(P, sh.G, stream);
+    if (pair) launch_t<64, 2, WALK, PAGED>(P, sh.G, stream);
+    else launch_t<64, 1, WALK, PAGED>(P, sh.G, stream);
   }
 }
 
-template <bool OSK>
+template <int WALK>
 hipError_t launch(const Shape& sh, const AttnArgs& a, hipStream_t stream) {
   AttnParams P;
   P.a = a;
@@ -506,11 +519,11 @@ hipError_t launch(const Shape& sh, const AttnArgs& a, hipStream_t stream) {
   P.n_units = sh.B * sh.Hkv * sh.nb;
   P.scale = sh.scale;
   P.scale_log2 = sh.scale * 1.4426950408889634f;
-  if constexpr (OSK) {
-    if (a.pg.table != nullptr) launch_shape<true, true>(sh, P, stream);
-    else launch_shape<true, false>(sh, P, stream);
+  if constexpr (WALK == kWalkList) {
+    if (a.pg.table != nullptr) launch_shape<kWalkList, true>(sh, P, stream);
+    else launch_shape<kWalkList, false>(sh, P, stream);
   } else {
-    launch_shape<false, false>(sh, P, stream);
+    launch_shape<WALK, false>(sh, P, stream);
   }
   return hipGetLastError();
 }
@@ -518,11 +531,15 @@ hipError_t launch(const Shape& sh, const AttnArgs& a, hipStream_t stream) {
 }  // namespace
 
 hipError_t launch_osk_attention(const Shape& sh, const AttnArgs& a, hipStream_t stream) {
-  return launch<true>(sh, a, stream);
+  return launch<kWalkList>(sh, a, stream);
 }
 
 hipError_t launch_dense_attention(const Shape& sh, const AttnArgs& a, hipStream_t stream) {
-  return launch<false>(sh, a, stream);
+  return launch<kWalkDense>(sh, a, stream);
+}
+
+hipError_t launch_masked_attention(const Shape& sh, const AttnArgs& a, hipStream_t stream) {
+  return launch<kWalkMask>(sh, a, stream);
 }
 
 }  // namespace cosa

@@ -333,6 +333,22 @@ cosa_status cosa_dense_attention(const cosa_problem* problem, const void* q, con
   return e == hipSuccess ? ok() : hip_fail(e, "dense_attention launch");
 }
 
+cosa_status cosa_masked_attention(const cosa_problem* problem, const void* q, const void* k,
+                                  const void* v, const uint8_t* mask, void* o, void* stream) {
+  cosa::Shape sh;
+  bool empty = false;
+  cosa_status st = make_shape(problem, sh, empty);
+  if (st != COSA_OK) return st;
+  if (empty) return ok();
+  if (!q || !k || !v || !mask || !o)
+    return fail(COSA_ERR_INVALID_ARG, "q, k, v, mask and o must be non-NULL");
+  cosa::AttnArgs a{static_cast<const uint16_t*>(q), static_cast<const uint16_t*>(k),
+                   static_cast<const uint16_t*>(v), static_cast<uint16_t*>(o), nullptr, nullptr,
+                   nullptr, nullptr, nullptr, 0, 0.f, cosa::KvPages{}, mask};
+  const hipError_t e = cosa::launch_masked_attention(sh, a, as_stream(stream));
+  return e == hipSuccess ? ok() : hip_fail(e, "masked_attention launch");
+}
+
 cosa_status cosa_prefill_workspace_layout(const cosa_problem* problem,
                                           cosa_workspace_layout* layout) {
   cosa::Shape sh;

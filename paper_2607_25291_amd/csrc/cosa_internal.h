@@ -58,6 +58,7 @@ struct AttnArgs {
   int skip_on;
   float tau;              // skip threshold in nats (float32)
   KvPages pg;             // k and v are the paged caches when pg.table != nullptr (OSK only)
+  const uint8_t* mask;    // block mask [B, Hkv, nb, nb] (masked walk only)
 };
 
 // LDS bytes the proxy-scoring kernel needs for a shape (0 if the shape is outside its limits).
@@ -68,5 +69,6 @@ hipError_t launch_kap_score(const Shape& sh, const KapScoreArgs& a, hipStream_t 
 hipError_t launch_kap_select(const Shape& sh, const KapSelectArgs& a, hipStream_t stream);
 hipError_t launch_osk_attention(const Shape& sh, const AttnArgs& a, hipStream_t stream);
 hipError_t launch_dense_attention(const Shape& sh, const AttnArgs& a, hipStream_t stream);
+hipError_t launch_masked_attention(const Shape& sh, const AttnArgs& a, hipStream_t stream);
 
 }  // namespace cosa

@@ -14,7 +14,7 @@ from paper_2607_25291_amd.calibrate import delta_for_budget
 EXPECTED = {"cosa_status_string", "cosa_last_error", "cosa_kap_score", "cosa_kap_select_ordered",
             "cosa_osk_attention", "cosa_dense_attention", "cosa_prefill_workspace_bytes",
             "cosa_prefill_workspace_layout", "cosa_prefill", "cosa_kap_score_paged",
-            "cosa_osk_attention_paged", "cosa_prefill_paged"}
+            "cosa_osk_attention_paged", "cosa_prefill_paged", "cosa_masked_attention"}
 
 
 def test_header_declares_the_abi():
@@ -124,6 +124,14 @@ def test_paged_validation():
     # the proxy alone does not need the V cache (an empty problem validates and launches nothing)
     B.cosa_kap_score_paged(B.Problem(0, 8, 2, 1024), None, kv(v=None), None, None, stream=0)
     B.cosa_prefill_paged(B.Problem(0, 8, 2, 1024), None, kv(), sel, None, None, 0, None, stream=0)
+    assert B.cosa_last_error() == ""
+
+
+def test_masked_attention_validation():
+    with pytest.raises(B.CosaError) as e:
+        B.cosa_masked_attention(GOOD, 16, 16, 16, None, 16, stream=0)
+    assert e.value.status == B.COSA_ERR_INVALID_ARG
+    B.cosa_masked_attention(B.Problem(0, 8, 2, 1024), None, None, None, None, None, stream=0)
     assert B.cosa_last_error() == ""
 
 
