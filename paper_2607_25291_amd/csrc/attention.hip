@@ -393,24 +393,34 @@ void attention_kernel(const AttnParams P) {
       // O^T += V^T P^T over 16-key chunks kc = 2 t + c2: P^T element e of the chunk is register
       // 8 c2 + e of tile t (key 32 t + 16 c2 + 8 (e / 4) + 4 half + e % 4); the V^T operand is the
       // matching pair of transposing reads (e / 4 = a).
+      // The transposing reads are issued directly so that the chunk and half-row offsets go into
+      // the instruction's offset field (the compiler adds them to the address in a VALU op per read
+      // otherwise); the explicit wait then hands the fragments to the MFMAs.
+      int va[4];
+#pragma unroll
+      for (int dt = 0; dt < 4; ++dt) va[dt] = (int)(size_t)COSA_LDS(Vb) + v_rd[dt];
 #pragma unroll
       for (int kc = 0; kc < BLOCK / 16; ++kc) {
         bf16x8_t pf;
 #pragma unroll
         for (int e = 0; e < 8; ++e) pf[e] = (__bf16)s[kc >> 1][8 * (kc & 1) + e];
-        bf16x8_t vf[4];
+        s16x4_t lo[4], hi[4];
 #pragma unroll
         for (int dt = 0; dt < 4; ++dt) {
-          const char* vp = Vb + v_rd[dt] + kc * 16 * 256;
-          const s16x4_t lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
-              (__attribute__((address_space(3))) s16x4_t*)(vp));
-          const s16x4_t hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
-              (__attribute__((address_space(3))) s16x4_t*)(vp + 8 * 256));
-          vf[dt] = __builtin_bit_cast(bf16x8_t,
-                                      __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
+          asm volatile("ds_read_b64_tr_b16 %0, %1 offset:%2"
+                       : "=v"(lo[dt]) : "v"(va[dt]), "i"(kc * 16 * 256));
+          asm volatile("ds_read_b64_tr_b16 %0, %1 offset:%2"
+                       : "=v"(hi[dt]) : "v"(va[dt]), "i"(kc * 16 * 256 + 8 * 256));
         }
+        asm volatile("s_waitcnt lgkmcnt(0)"
+                     : "+v"(lo[0]), "+v"(lo[1]), "+v"(lo[2]), "+v"(lo[3]), "+v"(hi[0]),
+                       "+v"(hi[1]), "+v"(hi[2]), "+v"(hi[3]));
 #pragma unroll
-        for (int dt = 0; dt < 4; ++dt) o[dt] = mfma32x32x16(vf[dt], pf, o[dt]);
+        for (int dt = 0; dt < 4; ++dt) {
+          const bf16x8_t vf = __builtin_bit_cast(
+              bf16x8_t, __builtin_shufflevector(lo[dt], hi[dt], 0, 1, 2, 3, 4, 5, 6, 7));
+          o[dt] = mfma32x32x16(vf, pf, o[dt]);
+        }
         __builtin_amdgcn_sched_group_barrier(0x100, 8, 0);  // the chunk's transposing reads ...
         __builtin_amdgcn_sched_group_barrier(0x008, 4, 0);  // ... then its MFMAs
       }
