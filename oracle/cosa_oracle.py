@@ -12,6 +12,7 @@ Sparse Attention" (arXiv 2607.25291):
 * Flag-grouped sort and the ordered mask M_KAP, Sec. 4.2 "Flag-grouped sorting", Eq. (mkap).
 * OSK list walk with in-kernel skip, Sec. 4.3 and Algorithm A, attention loop; skip rule Eq. (skip).
 * Dense attention, Sec. 3.1 (tiled online softmax = ordinary causal softmax attention).
+* Exact block attention mass (the ground truth of the proxy-fidelity comparison), Sec. 3.2.
 
 Readings of points where the paper is silent or loose (all indices 0-based):
 
@@ -381,6 +382,50 @@ def dense_attention(q_bits, k_bits, v_bits, *, block: int, sm_scale: float = 0.0
         else:
             o[(n, h, i)] = Oi
     return o
+
+
+def block_mass(q_bits, k_bits, *, n_kv_heads: int, block: int, sm_scale: float = 0.0,
+               units: Optional[Iterable[Tuple[int, int, int]]] = None):
+    """Exact attention mass that each query block puts on each key block, per KV group.
+
+    The ground truth behind the proxy-fidelity comparison of Sec. 3.2 (Property 1): the "oracle
+    mask" ranks the key blocks of a query block by the probability mass full attention assigns to
+    them. For batch n, KV head g, query block i and key block j <= i:
+        mass[n, g, i, j] = sum over the query heads h of group g and the rows r of block i of
+                           sum over the keys c of block j with c <= r of P_h[r, c],
+    with P_h[r, :] = softmax over the causal keys of sm_scale * Q_h[r] . K_g[c]. Each row's
+    probabilities sum to one, so the masses of row block i sum to G times its row count.
+    units=None: full array [B, Hkv, nb, nb] (entries j > i are 0); otherwise a dict
+    (n, g, i) -> float64 [i + 1].
+    """
+    qw, kw = _Heads(q_bits), _Heads(k_bits)
+    B, Hq, L, d = qw.shape
+    G = Hq // n_kv_heads
+    nb = n_blocks(L, block)
+    scale = default_scale(d, sm_scale)
+    full = units is None
+    if full:
+        units = [(n, g, i) for n in range(B) for g in range(n_kv_heads) for i in range(nb)]
+        out = np.zeros((B, n_kv_heads, nb, nb))
+    else:
+        out = {}
+    for (n, g, i) in units:
+        t0, t1 = _rows_of_block(i, block, L)
+        rows = np.arange(t0, t1)
+        keys = np.arange(0, t1)
+        acc = np.zeros(i + 1)
+        for h in range(g * G, (g + 1) * G):
+            S = scale * (qw(n, h)[rows] @ kw(n, g)[keys].T)
+            S[keys[None, :] > rows[:, None]] = -np.inf
+            P = np.exp(S - S.max(axis=1, keepdims=True))
+            P /= P.sum(axis=1, keepdims=True)
+            for j in range(i + 1):
+                acc[j] += P[:, j * block:min((j + 1) * block, L)].sum()
+        if full:
+            out[n, g, i, :i + 1] = acc
+        else:
+            out[(n, g, i)] = acc
+    return out
 
 
 # ----------------------------------------------------------------------------------------------
