@@ -3,6 +3,7 @@
     python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload qwen3_8b_l128k]
     python bench.py --sweep [--steps K]     # budget / visiting-order sweep (one JSON object)
     python bench.py --microbench [--steps K]  # list walk vs mask walk vs dense (one JSON object)
+    python bench.py --fidelity                # proxy fidelity and remapping sweep (one JSON object)
 
 A step is one pass of the whole hot path, cosa_prefill (proxy scoring, ordered selection, ordered-
 skipping attention) over one attention layer of synthetic bf16 inputs that are already resident in
@@ -291,6 +292,109 @@ def run_microbench(args):
     print(json.dumps({"steps": args.steps, "data": "synthetic", "records": recs}), flush=True)
 
 
+def run_fidelity(args):
+    """Synthetic fidelity analysis (Sec. 3.2 Property 1; Sec. 5.4 "Effect of remapping"; appendix D
+    "Full remapping sweep"), with exact attention on the GPU as the ground truth.
+
+    A. Proxy fidelity: for stage-1 budgets B1, the IoU between the blocks KAP keeps for a query
+       block and the same number of blocks with the largest exact attention mass (the oracle mask),
+       and the share of attention mass the kept set captures. Two host-side selections from the
+       same inputs give context: top blocks by KAP score alone (no HRM grouping) and the most recent
+       blocks (a local window).
+    B. Remapping: for B1 in {100, 54, 42, 32, 28} %, the in-kernel skip ratio and the output error
+       against dense attention as Delta varies, visiting blocks in KAP order (remapped) or ascending.
+    """
+    import torch
+    from paper_2607_25291_amd import binding as B
+    from paper_2607_25291_amd.inputs import WORKLOADS, make_inputs
+
+    w = WORKLOADS[args.fidelity_workload]
+    dev = torch.device("cuda:0")
+    p = B.Problem(w.batch, w.n_q_heads, w.n_kv_heads, w.seq_len, w.head_dim, w.block, w.stride)
+    nb, G, L = w.n_blocks, w.n_q_heads // w.n_kv_heads, w.seq_len
+    log(f"[fidelity] {w.name}: generating inputs")
+    q_np, k_np, v_np = make_inputs(w)
+    up = lambda a: torch.from_numpy(a.view(np.int16)).to(dev)
+    q, k, v = up(q_np), up(k_np), up(v_np)
+    shp = (w.batch, w.n_kv_heads, nb, nb)
+    mass_t = torch.zeros(shp, dtype=torch.float32, device=dev)
+    B.cosa_block_mass(p, q, k, mass_t)
+    score_t = torch.zeros(shp, dtype=torch.float32, device=dev)
+    hrm_t = torch.zeros(shp, dtype=torch.uint8, device=dev)
+    B.cosa_kap_score(p, q, k, score_t, hrm_t)
+    order_t = torch.zeros(shp, dtype=torch.int32, device=dev)
+    count_t = torch.zeros(shp[:3], dtype=torch.int32, device=dev)
+    mass, score = mass_t.cpu().numpy().astype(np.float64), score_t.cpu().numpy()
+    o_dense = torch.empty_like(q)
+    B.cosa_dense_attention(p, q, k, v, o_dense)
+    dense_f = o_dense.view(torch.bfloat16).float()
+    rows = [(n, g, i) for n in range(w.batch) for g in range(w.n_kv_heads) for i in range(nb)]
+    log(f"[fidelity] exact block mass and proxy scores ready ({len(rows)} query blocks per layer)")
+
+    def top(vals, kk):
+        # the kk largest entries (ties to the lower block index)
+        idx = np.lexsort((np.arange(vals.size), -vals))
+        return set(idx[:kk].tolist())
+
+    fid = []
+    for b1 in (0.02, 0.05, 0.10, 0.20, 0.40, 0.60):
+        B.cosa_kap_select_ordered(p, score_t, hrm_t, B.select(B.SELECT_FRACTION, b1), order_t,
+                                  count_t)
+        order, count = order_t.cpu().numpy(), count_t.cpu().numpy()
+        iou = {"kap": [], "score_only": [], "local": []}
+        cap = {"kap": [], "score_only": [], "local": [], "oracle": []}
+        for (n, g, i) in rows:
+            kk = int(count[n, g, i])
+            m = mass[n, g, i, :i + 1]
+            oracle = top(m, kk)
+            sets = {"kap": set(order[n, g, i, :kk].tolist()),
+                    "score_only": top(score[n, g, i, :i + 1].astype(np.float64), kk),
+                    "local": set(range(i + 1 - kk, i + 1))}
+            total = m.sum()
+            cap["oracle"].append(m[list(oracle)].sum() / total)
+            for key, st in sets.items():
+                iou[key].append(len(st & oracle) / len(st | oracle))
+                cap[key].append(m[list(st)].sum() / total)
+        rec = {"b1": b1, "realized_b1": round(float(count.sum()) / (w.batch * w.n_kv_heads * nb * (nb + 1) / 2), 5)}
+        for key in iou:
+            rec[f"iou_{key}"] = round(float(np.mean(iou[key])), 4)
+        for key in cap:
+            rec[f"mass_{key}"] = round(float(np.mean(cap[key])), 4)
+        log(f"[fidelity] {rec}")
+        fid.append(rec)
+
+    remap = []
+    deltas = [d for d in (10.0, 30.0, 100.0, 300.0, 1000.0, 3000.0, 10000.0) if d <= L]
+    o = torch.empty_like(q)
+    margin = torch.zeros((w.batch, w.n_q_heads, nb, nb), dtype=torch.float32, device=dev)
+    causal = w.batch * w.n_q_heads * nb * (nb + 1) // 2
+    for b1 in (1.00, 0.54, 0.42, 0.32, 0.28):
+        for mode, name in ((B.ORDER_KAP, "remapped"), (B.ORDER_ASCENDING, "ascending")):
+            sel = B.select(B.SELECT_FRACTION, b1, mode)
+            B.cosa_kap_select_ordered(p, score_t, hrm_t, sel, order_t, count_t)
+            margin.zero_()
+            B.cosa_osk_attention(p, q, k, v, order_t, count_t, None, o, None, margin, None)
+            cnt_q = np.repeat(count_t.cpu().numpy(), G, axis=1)
+            pos = np.arange(nb)[None, None, None, :] < cnt_q[..., None]
+            marg = margin.cpu().numpy()[pos]
+            listed = int(cnt_q.sum())
+            for delta in deltas:
+                tau = float(np.float32(math.log(float(np.float32(delta)) / L)))
+                skipped = int(np.count_nonzero(marg < tau))
+                B.cosa_osk_attention(p, q, k, v, order_t, count_t, B.skip(B.SKIP_ROWMAX, delta), o)
+                diff = (o.view(torch.bfloat16).float() - dense_f).abs()
+                rec = {"b1": b1, "order": name, "delta": delta,
+                       "skip_ratio": round(skipped / listed, 5),
+                       "overall_budget": round((listed - skipped) / causal, 5),
+                       "err_max": round(float(diff.max()), 5),
+                       "err_mean": round(float(diff.mean()), 6)}
+                remap.append(rec)
+            log(f"[fidelity] B1 {b1:.2f} {name}: skip ratios "
+                f"{[r['skip_ratio'] for r in remap[-len(deltas):]]}")
+    print(json.dumps({"workload": w.name, "data": "synthetic", "proxy_fidelity": fid,
+                      "remapping": remap}), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -305,6 +409,10 @@ def main():
     ap.add_argument("--microbench", action="store_true",
                     help="kernel microbenchmark: OSK list walk vs mask walk vs dense over "
                          "B in {25, 50, 75}% and L in {32K, 64K, 128K}")
+    ap.add_argument("--fidelity", action="store_true",
+                    help="proxy fidelity (IoU with the exact-mass oracle mask) and the remapping "
+                         "skip-ratio sweep, on --fidelity-workload")
+    ap.add_argument("--fidelity-workload", default="qwen3_8b_l32k")
     ap.add_argument("--sweep", action="store_true",
                     help="run the budget / visiting-order sweep instead of the one-line benchmark")
     ap.add_argument("--copy-probe-mib", type=int, default=0,
@@ -320,6 +428,9 @@ def main():
         return
     if args.microbench:
         run_microbench(args)
+        return
+    if args.fidelity:
+        run_fidelity(args)
         return
 
     import torch

@@ -201,6 +201,19 @@ cosa_status cosa_dense_attention(const cosa_problem* problem, const void* q, con
 cosa_status cosa_masked_attention(const cosa_problem* problem, const void* q, const void* k,
                                   const void* v, const uint8_t* mask, void* o, void* stream);
 
+/*
+ * Exact attention block mass per KV group (analysis; Sec. 3.2, Property 1: the mass that full
+ * attention puts on each key block defines the oracle mask a proxy is measured against).
+ *   mass[n, g, i, j] = sum over the query heads h of group g and the rows r of query block i of
+ *                      sum over the keys c of block j with c <= r of softmax_c(sm_scale Q_h[r].K_g[c])
+ * for j <= i (fp32 [B, Hkv, nb, nb]; entries j > i are not written). Each row's probabilities sum
+ * to one, so row block i's masses sum to G * b. Two passes over the keys per head (row statistics,
+ * then block sums); the summation order is fixed, so results are deterministic. Not on the
+ * prefill path: it costs about as much as dense attention.
+ */
+cosa_status cosa_block_mass(const cosa_problem* problem, const void* q, const void* k, float* mass,
+                            void* stream);
+
 /* Workspace size of cosa_prefill (0 if the problem is invalid; see cosa_last_error()). */
 size_t cosa_prefill_workspace_bytes(const cosa_problem* problem);
 

@@ -116,6 +116,8 @@ def lib():
         L.cosa_prefill.restype = S
         L.cosa_prefill.argtypes = [P, vp, vp, vp, ctypes.POINTER(CosaSelect),
                                    ctypes.POINTER(CosaSkip), vp, ctypes.c_size_t, vp, vp]
+        L.cosa_block_mass.restype = S
+        L.cosa_block_mass.argtypes = [P, vp, vp, vp, vp]
         L.cosa_masked_attention.restype = S
         L.cosa_masked_attention.argtypes = [P, vp, vp, vp, vp, vp, vp]
         KV = ctypes.POINTER(CosaPagedKv)
@@ -203,6 +205,11 @@ def cosa_dense_attention(problem, q, k, v, o, stream=None):
     p = _prob(problem)
     _check(lib().cosa_dense_attention(ctypes.byref(p), _ptr(q), _ptr(k), _ptr(v), _ptr(o),
                                       _stream(stream)))
+
+
+def cosa_block_mass(problem, q, k, mass, stream=None):
+    p = _prob(problem)
+    _check(lib().cosa_block_mass(ctypes.byref(p), _ptr(q), _ptr(k), _ptr(mass), _stream(stream)))
 
 
 def cosa_masked_attention(problem, q, k, v, mask, o, stream=None):

@@ -19,7 +19,7 @@ CSRC = os.path.join(PKG, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 BUILD = os.path.join(ROOT, "_build")
 LIB = os.path.join(PKG, "libcosa.so")
-SOURCES = ["cosa_api.hip", "attention.hip", "kap_score.hip", "kap_select.hip"]
+SOURCES = ["cosa_api.hip", "attention.hip", "kap_score.hip", "kap_select.hip", "block_mass.hip"]
 
 ARCH = "gfx950"
 COMMON = [

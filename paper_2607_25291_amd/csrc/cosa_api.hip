@@ -349,6 +349,22 @@ cosa_status cosa_masked_attention(const cosa_problem* problem, const void* q, co
   return e == hipSuccess ? ok() : hip_fail(e, "masked_attention launch");
 }
 
+cosa_status cosa_block_mass(const cosa_problem* problem, const void* q, const void* k, float* mass,
+                            void* stream) {
+  cosa::Shape sh;
+  bool empty = false;
+  cosa_status st = make_shape(problem, sh, empty);
+  if (st != COSA_OK) return st;
+  if (empty) return ok();
+  if (!q || !k || !mass) return fail(COSA_ERR_INVALID_ARG, "q, k and mass must be non-NULL");
+  if (cosa::block_mass_lds_bytes(sh) > 160 * 1024)
+    return fail(COSA_ERR_UNSUPPORTED, "%d blocks exceed the block-mass kernel's LDS", sh.nb);
+  const hipError_t e = cosa::launch_block_mass(sh, static_cast<const uint16_t*>(q),
+                                               static_cast<const uint16_t*>(k), mass,
+                                               as_stream(stream));
+  return e == hipSuccess ? ok() : hip_fail(e, "block_mass launch");
+}
+
 cosa_status cosa_prefill_workspace_layout(const cosa_problem* problem,
                                           cosa_workspace_layout* layout) {
   cosa::Shape sh;

@@ -70,5 +70,8 @@ hipError_t launch_kap_select(const Shape& sh, const KapSelectArgs& a, hipStream_
 hipError_t launch_osk_attention(const Shape& sh, const AttnArgs& a, hipStream_t stream);
 hipError_t launch_dense_attention(const Shape& sh, const AttnArgs& a, hipStream_t stream);
 hipError_t launch_masked_attention(const Shape& sh, const AttnArgs& a, hipStream_t stream);
+size_t block_mass_lds_bytes(const Shape& sh);
+hipError_t launch_block_mass(const Shape& sh, const uint16_t* q, const uint16_t* k, float* mass,
+                             hipStream_t stream);
 
 }  // namespace cosa

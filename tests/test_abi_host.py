@@ -14,7 +14,8 @@ from paper_2607_25291_amd.calibrate import delta_for_budget
 EXPECTED = {"cosa_status_string", "cosa_last_error", "cosa_kap_score", "cosa_kap_select_ordered",
             "cosa_osk_attention", "cosa_dense_attention", "cosa_prefill_workspace_bytes",
             "cosa_prefill_workspace_layout", "cosa_prefill", "cosa_kap_score_paged",
-            "cosa_osk_attention_paged", "cosa_prefill_paged", "cosa_masked_attention"}
+            "cosa_osk_attention_paged", "cosa_prefill_paged", "cosa_masked_attention",
+            "cosa_block_mass"}
 
 
 def test_header_declares_the_abi():
