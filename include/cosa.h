@@ -132,6 +132,27 @@ typedef struct {
   int64_t n_pages;
 } cosa_paged_kv;
 
+/*
+ * Variable-length packing. Several sequences of different lengths share one call by being
+ * concatenated along the token axis of the [B, H, L, d] tensors, each starting on a block boundary
+ * and spanning whole blocks: sequence q owns blocks [cu_blocks[q], cu_blocks[q + 1]) (tokens
+ * cu_blocks[q] * b .. cu_blocks[q + 1] * b - 1) of every batch entry. Each sequence is an
+ * independent causal problem: query block i of sequence q only sees key blocks from cu_blocks[q]
+ * up to i (proxy candidates, the stage-1 cut K_i over those i - cu_blocks[q] + 1 candidates, list
+ * entries, dense walk), and its skip threshold is ln(delta / L_q) with L_q its own length in tokens
+ * (Eq. (skip), N the context length of the sequence). The results for a sequence equal those of a
+ * separate call on that sequence alone, with block indices offset by cu_blocks[q].
+ *   n_seqs:    1 <= n_seqs <= COSA_MAX_PACKED_SEQS.
+ *   cu_blocks: HOST int32 [n_seqs + 1], cu_blocks[0] = 0, strictly increasing,
+ *              cu_blocks[n_seqs] = seq_len / block. Read during the call only.
+ * With skipping on, delta must not exceed the shortest sequence's length.
+ */
+#define COSA_MAX_PACKED_SEQS 128
+typedef struct {
+  int32_t n_seqs;
+  const int32_t* cu_blocks;
+} cosa_varlen;
+
 /* Human-readable name of a status code (static storage). */
 const char* cosa_status_string(cosa_status status);
 
@@ -254,6 +275,36 @@ cosa_status cosa_osk_attention_paged(const cosa_problem* problem, const void* q,
 cosa_status cosa_prefill_paged(const cosa_problem* problem, const void* q, const cosa_paged_kv* kv,
                                const cosa_select* select, const cosa_skip* skip, void* workspace,
                                size_t workspace_bytes, void* o, void* stream);
+
+/*
+ * Packed variable-length forms (cosa_varlen). Each behaves as the call without the suffix applied
+ * to every packed sequence separately; proxy entries (score, hrm, order rows) outside a block's own
+ * sequence are not read and, for score and hrm, not written.
+ */
+cosa_status cosa_kap_score_varlen(const cosa_problem* problem, const cosa_varlen* varlen,
+                                  const void* q, const void* k, float* score, uint8_t* hrm,
+                                  void* stream);
+cosa_status cosa_kap_select_ordered_varlen(const cosa_problem* problem, const cosa_varlen* varlen,
+                                           const float* score, const uint8_t* hrm,
+                                           const cosa_select* select, int32_t* order,
+                                           int32_t* count, void* stream);
+cosa_status cosa_osk_attention_varlen(const cosa_problem* problem, const cosa_varlen* varlen,
+                                      const void* q, const void* k, const void* v,
+                                      const int32_t* order, const int32_t* count,
+                                      const cosa_skip* skip, void* o, uint8_t* visit_log,
+                                      float* margin_log, int32_t* n_computed, void* stream);
+cosa_status cosa_dense_attention_varlen(const cosa_problem* problem, const cosa_varlen* varlen,
+                                        const void* q, const void* k, const void* v, void* o,
+                                        void* stream);
+cosa_status cosa_prefill_varlen(const cosa_problem* problem, const cosa_varlen* varlen,
+                                const void* q, const void* k, const void* v,
+                                const cosa_select* select, const cosa_skip* skip, void* workspace,
+                                size_t workspace_bytes, void* o, void* stream);
+cosa_status cosa_prefill_paged_varlen(const cosa_problem* problem, const cosa_varlen* varlen,
+                                      const void* q, const cosa_paged_kv* kv,
+                                      const cosa_select* select, const cosa_skip* skip,
+                                      void* workspace, size_t workspace_bytes, void* o,
+                                      void* stream);
 
 #ifdef __cplusplus
 }

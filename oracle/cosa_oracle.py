@@ -13,6 +13,8 @@ Sparse Attention" (arXiv 2607.25291):
 * OSK list walk with in-kernel skip, Sec. 4.3 and Algorithm A, attention loop; skip rule Eq. (skip).
 * Dense attention, Sec. 3.1 (tiled online softmax = ordinary causal softmax attention).
 * Exact block attention mass (the ground truth of the proxy-fidelity comparison), Sec. 3.2.
+* Packed variable-length batches: every packed sequence is its own problem (the definition; the
+  paper treats one sequence at a time), with N in ln(Delta/N) the sequence's own length.
 
 Readings of points where the paper is silent or loose (all indices 0-based):
 
@@ -470,3 +472,74 @@ def calibrate_delta(margins: np.ndarray, *, listed: int, total_causal: int, targ
         tau = 0.5 * (m[n_skip - 1] + hi)
     delta = seq_len * math.exp(tau)
     return float(delta), n_skip
+
+
+# ----------------------------------------------------------------------------------------------
+# Packed variable-length batches: independent causal sequences along one token axis
+# ----------------------------------------------------------------------------------------------
+def packed_spans(cu_blocks: Sequence[int], block: int) -> List[Tuple[int, int, int, int]]:
+    """(first block F, end block E, first token, end token) of every packed sequence; sequence q
+    owns blocks [cu_blocks[q], cu_blocks[q + 1])."""
+    cu = [int(x) for x in cu_blocks]
+    return [(cu[q], cu[q + 1], cu[q] * block, cu[q + 1] * block) for q in range(len(cu) - 1)]
+
+
+def prefill_varlen(q_bits, k_bits, v_bits, cu_blocks, *, n_kv_heads: int, block: int, stride: int,
+                   sm_scale: float = 0.0, select_mode: int = SELECT_FRACTION,
+                   select_value: float = 1.0, order_mode: int = ORDER_KAP,
+                   skip_mode: int = SKIP_NONE, delta: float = 0.0):
+    """Algorithm A on a pack of sequences, each one its own causal prefill problem.
+
+    The proxy (Eq. (score)), the stage-1 cut (Eq. (mkap)) and the OSK walk (Eq. (skip), with N the
+    sequence's own length in the threshold ln(Delta/N)) run on the tokens of one sequence alone;
+    their block indices are then shifted by the sequence's first block into the packed arrays.
+    Entries that pair blocks of different sequences stay at the unit-not-computed values (score
+    NaN, hrm 255) and -1 in the order rows.
+    """
+    B, Hq, L, d = q_bits.shape
+    nb = n_blocks(L, block)
+    score = np.full((B, n_kv_heads, nb, nb), np.nan)
+    hrm = np.full((B, n_kv_heads, nb, nb), 255, dtype=np.uint8)
+    order = np.full((B, n_kv_heads, nb, nb), -1, dtype=np.int32)
+    count = np.zeros((B, n_kv_heads, nb), dtype=np.int32)
+    o = np.full((B, Hq, L, d), np.nan)
+    visit = np.zeros((B, Hq, nb, nb), dtype=np.uint8)
+    margin = np.full((B, Hq, nb, nb), np.nan)
+    ncomp = np.full((B, Hq, nb), -1, dtype=np.int32)
+    taus = []
+    for (F, E, t0, t1) in packed_spans(cu_blocks, block):
+        qs = np.ascontiguousarray(q_bits[:, :, t0:t1])
+        ks = np.ascontiguousarray(k_bits[:, :, t0:t1])
+        vs = np.ascontiguousarray(v_bits[:, :, t0:t1])
+        sc, hr = kap_score(qs, ks, n_kv_heads=n_kv_heads, block=block, stride=stride,
+                           sm_scale=sm_scale)
+        od, ct = kap_select(sc, hr, mode=select_mode, value=select_value, order_mode=order_mode)
+        res = osk_attention(qs, ks, vs, od, ct, block=block, sm_scale=sm_scale,
+                            skip_mode=skip_mode, delta=delta)
+        n_q = E - F
+        for i in range(n_q):
+            score[:, :, F + i, F:F + i + 1] = sc[:, :, i, :i + 1]
+            hrm[:, :, F + i, F:F + i + 1] = hr[:, :, i, :i + 1]
+        shifted = np.where(od >= 0, od + F, -1).astype(np.int32)
+        order[:, :, F:E, :n_q] = shifted
+        count[:, :, F:E] = ct
+        o[:, :, t0:t1] = res["o"]
+        visit[:, :, F:E, :n_q] = res["visit"]
+        margin[:, :, F:E, :n_q] = res["margin"]
+        ncomp[:, :, F:E] = res["n_computed"]
+        taus.append(res["tau"])
+    return {"score": score, "hrm": hrm, "order": order, "count": count, "o": o, "visit": visit,
+            "margin": margin, "n_computed": ncomp, "tau": taus}
+
+
+def dense_attention_varlen(q_bits, k_bits, v_bits, cu_blocks, *, block: int,
+                           sm_scale: float = 0.0):
+    """Causal softmax attention within each packed sequence (Sec. 3.1 per sequence)."""
+    B, Hq, L, d = q_bits.shape
+    o = np.full((B, Hq, L, d), np.nan)
+    for (F, E, t0, t1) in packed_spans(cu_blocks, block):
+        o[:, :, t0:t1] = dense_attention(np.ascontiguousarray(q_bits[:, :, t0:t1]),
+                                         np.ascontiguousarray(k_bits[:, :, t0:t1]),
+                                         np.ascontiguousarray(v_bits[:, :, t0:t1]), block=block,
+                                         sm_scale=sm_scale)
+    return o

@@ -50,6 +50,13 @@ class CosaPagedKv(ctypes.Structure):
                 ("n_pages", ctypes.c_int64)]
 
 
+class CosaVarlen(ctypes.Structure):
+    _fields_ = [("n_seqs", ctypes.c_int32), ("cu_blocks", ctypes.POINTER(ctypes.c_int32))]
+
+
+MAX_PACKED_SEQS = 128
+
+
 class CosaError(RuntimeError):
     def __init__(self, status: int, message: str):
         super().__init__(message)
@@ -129,6 +136,24 @@ def lib():
         L.cosa_prefill_paged.restype = S
         L.cosa_prefill_paged.argtypes = [P, vp, KV, ctypes.POINTER(CosaSelect),
                                          ctypes.POINTER(CosaSkip), vp, ctypes.c_size_t, vp, vp]
+        VL = ctypes.POINTER(CosaVarlen)
+        L.cosa_kap_score_varlen.restype = S
+        L.cosa_kap_score_varlen.argtypes = [P, VL, vp, vp, vp, vp, vp]
+        L.cosa_kap_select_ordered_varlen.restype = S
+        L.cosa_kap_select_ordered_varlen.argtypes = [P, VL, vp, vp, ctypes.POINTER(CosaSelect), vp,
+                                                     vp, vp]
+        L.cosa_osk_attention_varlen.restype = S
+        L.cosa_osk_attention_varlen.argtypes = [P, VL, vp, vp, vp, vp, vp, ctypes.POINTER(CosaSkip),
+                                                vp, vp, vp, vp, vp]
+        L.cosa_dense_attention_varlen.restype = S
+        L.cosa_dense_attention_varlen.argtypes = [P, VL, vp, vp, vp, vp, vp]
+        L.cosa_prefill_varlen.restype = S
+        L.cosa_prefill_varlen.argtypes = [P, VL, vp, vp, vp, ctypes.POINTER(CosaSelect),
+                                          ctypes.POINTER(CosaSkip), vp, ctypes.c_size_t, vp, vp]
+        L.cosa_prefill_paged_varlen.restype = S
+        L.cosa_prefill_paged_varlen.argtypes = [P, VL, vp, KV, ctypes.POINTER(CosaSelect),
+                                                ctypes.POINTER(CosaSkip), vp, ctypes.c_size_t, vp,
+                                                vp]
         _lib = L
     return _lib
 
@@ -272,3 +297,66 @@ def cosa_prefill_paged(problem, q, kv: CosaPagedKv, sel: CosaSelect, sk: Optiona
     _check(lib().cosa_prefill_paged(ctypes.byref(p), _ptr(q), _kvref(kv), ctypes.byref(sel),
                                     skp, _ptr(workspace), workspace_bytes, _ptr(o),
                                     _stream(stream)))
+
+
+def varlen(cu_blocks) -> CosaVarlen:
+    """cosa_varlen from host block offsets [0, ..., nb] of the packed sequences (the struct keeps
+    its own copy of the array alive)."""
+    vals = [int(x) for x in cu_blocks]
+    arr = (ctypes.c_int32 * max(len(vals), 1))(*vals)
+    v = CosaVarlen(len(vals) - 1, ctypes.cast(arr, ctypes.POINTER(ctypes.c_int32)))
+    v._host_offsets = arr
+    return v
+
+
+def _vlref(vl):
+    return ctypes.byref(vl) if vl is not None else None
+
+
+def cosa_kap_score_varlen(problem, vl: CosaVarlen, q, k, score, hrm, stream=None):
+    p = _prob(problem)
+    _check(lib().cosa_kap_score_varlen(ctypes.byref(p), _vlref(vl), _ptr(q), _ptr(k), _ptr(score),
+                                       _ptr(hrm), _stream(stream)))
+
+
+def cosa_kap_select_ordered_varlen(problem, vl: CosaVarlen, score, hrm, sel: CosaSelect, order,
+                                   count, stream=None):
+    p = _prob(problem)
+    _check(lib().cosa_kap_select_ordered_varlen(ctypes.byref(p), _vlref(vl), _ptr(score), _ptr(hrm),
+                                                ctypes.byref(sel), _ptr(order), _ptr(count),
+                                                _stream(stream)))
+
+
+def cosa_osk_attention_varlen(problem, vl: CosaVarlen, q, k, v, order, count,
+                              sk: Optional[CosaSkip], o, visit_log=None, margin_log=None,
+                              n_computed=None, stream=None):
+    p = _prob(problem)
+    skp = ctypes.byref(sk) if sk is not None else None
+    _check(lib().cosa_osk_attention_varlen(ctypes.byref(p), _vlref(vl), _ptr(q), _ptr(k), _ptr(v),
+                                           _ptr(order), _ptr(count), skp, _ptr(o), _ptr(visit_log),
+                                           _ptr(margin_log), _ptr(n_computed), _stream(stream)))
+
+
+def cosa_dense_attention_varlen(problem, vl: CosaVarlen, q, k, v, o, stream=None):
+    p = _prob(problem)
+    _check(lib().cosa_dense_attention_varlen(ctypes.byref(p), _vlref(vl), _ptr(q), _ptr(k), _ptr(v),
+                                             _ptr(o), _stream(stream)))
+
+
+def cosa_prefill_varlen(problem, vl: CosaVarlen, q, k, v, sel: CosaSelect, sk: Optional[CosaSkip],
+                        workspace, workspace_bytes: int, o, stream=None):
+    p = _prob(problem)
+    skp = ctypes.byref(sk) if sk is not None else None
+    _check(lib().cosa_prefill_varlen(ctypes.byref(p), _vlref(vl), _ptr(q), _ptr(k), _ptr(v),
+                                     ctypes.byref(sel), skp, _ptr(workspace), workspace_bytes,
+                                     _ptr(o), _stream(stream)))
+
+
+def cosa_prefill_paged_varlen(problem, vl: CosaVarlen, q, kv: CosaPagedKv, sel: CosaSelect,
+                              sk: Optional[CosaSkip], workspace, workspace_bytes: int, o,
+                              stream=None):
+    p = _prob(problem)
+    skp = ctypes.byref(sk) if sk is not None else None
+    _check(lib().cosa_prefill_paged_varlen(ctypes.byref(p), _vlref(vl), _ptr(q), _kvref(kv),
+                                           ctypes.byref(sel), skp, _ptr(workspace),
+                                           workspace_bytes, _ptr(o), _stream(stream)))

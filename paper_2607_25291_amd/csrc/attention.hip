@@ -176,6 +176,12 @@ void attention_kernel(const AttnParams P) {
   const __amdgpu_buffer_rsrc_t vrs = __builtin_amdgcn_make_buffer_rsrc(
       (void*)(P.a.v + kv_off), (short)0, P.L * kHeadDim * 2, 0x00020000);
 
+  // Packed sequences: block i only sees the blocks F .. i of its own sequence, whose skip
+  // threshold is its own (F = 0 and the call's threshold without packing; the masked walk is
+  // never packed).
+  int seq;
+  const int F = pack_first(P.a.pack, i, seq);
+  const float tau = P.a.pack.n > 0 ? P.a.pack.tau[seq] : P.a.tau;
   int cnt;
   const int32_t* lst = nullptr;
   const uint8_t* mrow = nullptr;
@@ -184,19 +190,19 @@ void attention_kernel(const AttnParams P) {
     cnt = cnt < P.nb ? cnt : P.nb;
     lst = P.a.order + ((size_t)ng * P.nb + i) * P.nb;
   } else {
-    cnt = i + 1;
+    cnt = i - F + 1;
     if constexpr (MASKED) mrow = P.a.mask + ((size_t)ng * P.nb + i) * P.nb;
   }
-  // List entries, read ahead of their use. A malformed entry (outside [0, i]) is fetched as block
+  // List entries, read ahead of their use. A malformed entry (outside [F, i]) is fetched as block
   // i but contributes nothing. With a block mask, a masked block's entry is -1: nothing is fetched
   // or computed for it, but the walk still steps through it (logical skipping).
   auto raw_entry = [&](int kk) -> int {
     if constexpr (OSK) return kk < cnt ? lst[kk] : 0;
     else if constexpr (MASKED) return (kk < cnt && mrow[kk] != 0) ? kk : -1;
-    else return kk;
+    else return F + kk;
   };
-  auto listed = [&](int raw) -> bool { return (unsigned)raw <= (unsigned)i; };
-  auto page_of = [&](int raw) -> int { return (unsigned)raw <= (unsigned)i ? raw : i; };
+  auto listed = [&](int raw) -> bool { return (unsigned)(raw - F) <= (unsigned)(i - F); };
+  auto page_of = [&](int raw) -> int { return listed(raw) ? raw : i; };
 
   // Physical pages of a listed block (paged caches): lane k loads the page of the block's k-th
   // page-sized segment; entries outside [0, n_pages) read page 0.
@@ -362,7 +368,7 @@ void attention_kernel(const AttnParams P) {
         float dk = vote[BUF][hw * WPH];
 #pragma unroll
         for (int ww = 1; ww < WPH; ++ww) dk = fmaxf(dk, vote[BUF][hw * WPH + ww]);
-        skip = P.a.skip_on && (dk < P.a.tau);
+        skip = P.a.skip_on && (dk < tau);
         if (wl == 0 && lane == 0) {
           if (P.a.visit_log) P.a.visit_log[log_off + kk] = skip ? 2 : 1;
           if (P.a.margin_log) P.a.margin_log[log_off + kk] = dk;

@@ -9,6 +9,8 @@
 #include "cosa.h"
 #include "cosa_internal.h"
 
+static_assert(COSA_MAX_PACKED_SEQS == cosa::kMaxPackedSeqs, "packing limit of the ABI and kernels");
+
 namespace {
 
 thread_local std::string g_last_error;
@@ -145,6 +147,40 @@ cosa_status check_paged(const cosa_paged_kv* kv, const cosa::Shape& sh, bool nee
   return ok();
 }
 
+// Validates a packing of several sequences along the token axis and fills the kernel-argument form:
+// block offsets and, with skipping on, each sequence's threshold ln(Delta / L_q) (Eq. (skip) with N
+// the sequence's own length), computed in double and rounded once to float.
+cosa_status check_varlen(const cosa_varlen* vl, const cosa::Shape& sh, const cosa_skip* sk,
+                         cosa::SeqPack& sp) {
+  if (!vl) return fail(COSA_ERR_INVALID_ARG, "varlen is NULL");
+  if (vl->n_seqs < 1 || vl->n_seqs > COSA_MAX_PACKED_SEQS)
+    return fail(COSA_ERR_INVALID_ARG, "n_seqs %d outside [1, %d]", vl->n_seqs,
+                COSA_MAX_PACKED_SEQS);
+  if (!vl->cu_blocks) return fail(COSA_ERR_INVALID_ARG, "cu_blocks is NULL");
+  if (vl->cu_blocks[0] != 0)
+    return fail(COSA_ERR_INVALID_ARG, "cu_blocks[0] = %d, must be 0", vl->cu_blocks[0]);
+  for (int q = 0; q < vl->n_seqs; ++q)
+    if (vl->cu_blocks[q + 1] <= vl->cu_blocks[q])
+      return fail(COSA_ERR_INVALID_ARG, "cu_blocks must increase strictly (entries %d and %d)", q,
+                  q + 1);
+  if (vl->cu_blocks[vl->n_seqs] != sh.nb)
+    return fail(COSA_ERR_INVALID_ARG, "cu_blocks[n_seqs] = %d, must equal seq_len / block = %d",
+                vl->cu_blocks[vl->n_seqs], sh.nb);
+  sp = cosa::SeqPack{};
+  sp.n = vl->n_seqs;
+  for (int q = 0; q <= vl->n_seqs; ++q) sp.cu[q] = vl->cu_blocks[q];
+  if (sk && sk->mode == COSA_SKIP_ROWMAX) {
+    for (int q = 0; q < vl->n_seqs; ++q) {
+      const long long len = (long long)(sp.cu[q + 1] - sp.cu[q]) * sh.b;
+      if ((double)sk->delta > (double)len)
+        return fail(COSA_ERR_INVALID_ARG, "skip delta %g exceeds the length %lld of sequence %d",
+                    (double)sk->delta, len, q);
+      sp.tau[q] = (float)log((double)sk->delta / (double)len);
+    }
+  }
+  return ok();
+}
+
 size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 
 cosa_workspace_layout layout_of(const cosa::Shape& sh) {
@@ -161,10 +197,11 @@ cosa_workspace_layout layout_of(const cosa::Shape& sh) {
 
 hipStream_t as_stream(void* s) { return reinterpret_cast<hipStream_t>(s); }
 
-// Algorithm A end to end; kv == nullptr: contiguous K and V at k, v.
+// Algorithm A end to end; kv == nullptr: contiguous K and V at k, v; vl == nullptr: no packing.
 cosa_status prefill(const cosa_problem* problem, const void* q, const void* k, const void* v,
-                    const cosa_paged_kv* kv, const cosa_select* select, const cosa_skip* skip,
-                    void* workspace, size_t workspace_bytes, void* o, void* stream) {
+                    const cosa_paged_kv* kv, const cosa_varlen* vl, const cosa_select* select,
+                    const cosa_skip* skip, void* workspace, size_t workspace_bytes, void* o,
+                    void* stream) {
   cosa::Shape sh;
   bool empty = false;
   cosa_status st = make_shape(problem, sh, empty);
@@ -177,6 +214,8 @@ cosa_status prefill(const cosa_problem* problem, const void* q, const void* k, c
   cosa::KvPages pg{};
   if (kv && (st = check_paged(kv, sh, true, pg)) != COSA_OK) return st;
   if (empty) return ok();
+  cosa::SeqPack sp{};
+  if (vl && (st = check_varlen(vl, sh, skip, sp)) != COSA_OK) return st;
   if ((st = check_proxy_limits(sh)) != COSA_OK) return st;
   if (!q || !k || !v || !o) return fail(COSA_ERR_INVALID_ARG, "q, k, v and o must be non-NULL");
   const cosa_workspace_layout l = layout_of(sh);
@@ -191,16 +230,17 @@ cosa_status prefill(const cosa_problem* problem, const void* q, const void* k, c
   const hipStream_t s = as_stream(stream);
   hipError_t e = cosa::launch_kap_score(
       sh, cosa::KapScoreArgs{static_cast<const uint16_t*>(q), static_cast<const uint16_t*>(k), score,
-                             hrm, pg},
+                             hrm, pg, sp},
       s);
   if (e != hipSuccess) return hip_fail(e, "kap_score launch");
   e = cosa::launch_kap_select(
-      sh, cosa::KapSelectArgs{score, hrm, order, count, (int)select->mode, (int)select->order, micro},
+      sh,
+      cosa::KapSelectArgs{score, hrm, order, count, (int)select->mode, (int)select->order, micro, sp},
       s);
   if (e != hipSuccess) return hip_fail(e, "kap_select launch");
   cosa::AttnArgs a{static_cast<const uint16_t*>(q), static_cast<const uint16_t*>(k),
                    static_cast<const uint16_t*>(v), static_cast<uint16_t*>(o), order, count,
-                   nullptr, nullptr, nullptr, on, tau, pg};
+                   nullptr, nullptr, nullptr, on, tau, pg, nullptr, sp};
   e = cosa::launch_osk_attention(sh, a, s);
   return e == hipSuccess ? ok() : hip_fail(e, "osk_attention launch");
 }
@@ -385,14 +425,116 @@ size_t cosa_prefill_workspace_bytes(const cosa_problem* problem) {
 cosa_status cosa_prefill(const cosa_problem* problem, const void* q, const void* k, const void* v,
                          const cosa_select* select, const cosa_skip* skip, void* workspace,
                          size_t workspace_bytes, void* o, void* stream) {
-  return prefill(problem, q, k, v, nullptr, select, skip, workspace, workspace_bytes, o, stream);
+  return prefill(problem, q, k, v, nullptr, nullptr, select, skip, workspace, workspace_bytes, o,
+                 stream);
 }
 
 cosa_status cosa_prefill_paged(const cosa_problem* problem, const void* q, const cosa_paged_kv* kv,
                                const cosa_select* select, const cosa_skip* skip, void* workspace,
                                size_t workspace_bytes, void* o, void* stream) {
   if (!kv) return fail(COSA_ERR_INVALID_ARG, "paged kv is NULL");
-  return prefill(problem, q, kv->k_cache, kv->v_cache, kv, select, skip, workspace,
+  return prefill(problem, q, kv->k_cache, kv->v_cache, kv, nullptr, select, skip, workspace,
+                 workspace_bytes, o, stream);
+}
+
+cosa_status cosa_kap_score_varlen(const cosa_problem* problem, const cosa_varlen* varlen,
+                                  const void* q, const void* k, float* score, uint8_t* hrm,
+                                  void* stream) {
+  cosa::Shape sh;
+  bool empty = false;
+  cosa_status st = make_shape(problem, sh, empty);
+  if (st != COSA_OK) return st;
+  if (empty) return ok();
+  cosa::SeqPack sp{};
+  if ((st = check_varlen(varlen, sh, nullptr, sp)) != COSA_OK) return st;
+  if ((st = check_proxy_limits(sh)) != COSA_OK) return st;
+  if (!q || !k || !score || !hrm)
+    return fail(COSA_ERR_INVALID_ARG, "q, k, score and hrm must be non-NULL");
+  cosa::KapScoreArgs a{static_cast<const uint16_t*>(q), static_cast<const uint16_t*>(k), score, hrm,
+                       cosa::KvPages{}, sp};
+  const hipError_t e = cosa::launch_kap_score(sh, a, as_stream(stream));
+  return e == hipSuccess ? ok() : hip_fail(e, "kap_score launch");
+}
+
+cosa_status cosa_kap_select_ordered_varlen(const cosa_problem* problem, const cosa_varlen* varlen,
+                                           const float* score, const uint8_t* hrm,
+                                           const cosa_select* select, int32_t* order,
+                                           int32_t* count, void* stream) {
+  cosa::Shape sh;
+  bool empty = false;
+  cosa_status st = make_shape(problem, sh, empty);
+  if (st != COSA_OK) return st;
+  int64_t micro = 0;
+  if ((st = check_select(select, micro)) != COSA_OK) return st;
+  if (empty) return ok();
+  cosa::SeqPack sp{};
+  if ((st = check_varlen(varlen, sh, nullptr, sp)) != COSA_OK) return st;
+  if (!score || !hrm || !order || !count)
+    return fail(COSA_ERR_INVALID_ARG, "score, hrm, order and count must be non-NULL");
+  cosa::KapSelectArgs a{score, hrm, order, count, (int)select->mode, (int)select->order, micro, sp};
+  const hipError_t e = cosa::launch_kap_select(sh, a, as_stream(stream));
+  return e == hipSuccess ? ok() : hip_fail(e, "kap_select launch");
+}
+
+cosa_status cosa_osk_attention_varlen(const cosa_problem* problem, const cosa_varlen* varlen,
+                                      const void* q, const void* k, const void* v,
+                                      const int32_t* order, const int32_t* count,
+                                      const cosa_skip* skip, void* o, uint8_t* visit_log,
+                                      float* margin_log, int32_t* n_computed, void* stream) {
+  cosa::Shape sh;
+  bool empty = false;
+  cosa_status st = make_shape(problem, sh, empty);
+  if (st != COSA_OK) return st;
+  int on = 0;
+  float tau = 0.f;
+  if ((st = check_skip(skip, sh, on, tau)) != COSA_OK) return st;
+  if (empty) return ok();
+  cosa::SeqPack sp{};
+  if ((st = check_varlen(varlen, sh, skip, sp)) != COSA_OK) return st;
+  if (!q || !k || !v || !order || !count || !o)
+    return fail(COSA_ERR_INVALID_ARG, "q, k, v, order, count and o must be non-NULL");
+  cosa::AttnArgs a{static_cast<const uint16_t*>(q), static_cast<const uint16_t*>(k),
+                   static_cast<const uint16_t*>(v), static_cast<uint16_t*>(o), order, count,
+                   visit_log, margin_log, n_computed, on, tau, cosa::KvPages{}, nullptr, sp};
+  const hipError_t e = cosa::launch_osk_attention(sh, a, as_stream(stream));
+  return e == hipSuccess ? ok() : hip_fail(e, "osk_attention launch");
+}
+
+cosa_status cosa_dense_attention_varlen(const cosa_problem* problem, const cosa_varlen* varlen,
+                                        const void* q, const void* k, const void* v, void* o,
+                                        void* stream) {
+  cosa::Shape sh;
+  bool empty = false;
+  cosa_status st = make_shape(problem, sh, empty);
+  if (st != COSA_OK) return st;
+  if (empty) return ok();
+  cosa::SeqPack sp{};
+  if ((st = check_varlen(varlen, sh, nullptr, sp)) != COSA_OK) return st;
+  if (!q || !k || !v || !o) return fail(COSA_ERR_INVALID_ARG, "q, k, v and o must be non-NULL");
+  cosa::AttnArgs a{static_cast<const uint16_t*>(q), static_cast<const uint16_t*>(k),
+                   static_cast<const uint16_t*>(v), static_cast<uint16_t*>(o), nullptr, nullptr,
+                   nullptr, nullptr, nullptr, 0, 0.f, cosa::KvPages{}, nullptr, sp};
+  const hipError_t e = cosa::launch_dense_attention(sh, a, as_stream(stream));
+  return e == hipSuccess ? ok() : hip_fail(e, "dense_attention launch");
+}
+
+cosa_status cosa_prefill_varlen(const cosa_problem* problem, const cosa_varlen* varlen,
+                                const void* q, const void* k, const void* v,
+                                const cosa_select* select, const cosa_skip* skip, void* workspace,
+                                size_t workspace_bytes, void* o, void* stream) {
+  if (!varlen) return fail(COSA_ERR_INVALID_ARG, "varlen is NULL");
+  return prefill(problem, q, k, v, nullptr, varlen, select, skip, workspace, workspace_bytes, o,
+                 stream);
+}
+
+cosa_status cosa_prefill_paged_varlen(const cosa_problem* problem, const cosa_varlen* varlen,
+                                      const void* q, const cosa_paged_kv* kv,
+                                      const cosa_select* select, const cosa_skip* skip,
+                                      void* workspace, size_t workspace_bytes, void* o,
+                                      void* stream) {
+  if (!kv) return fail(COSA_ERR_INVALID_ARG, "paged kv is NULL");
+  if (!varlen) return fail(COSA_ERR_INVALID_ARG, "varlen is NULL");
+  return prefill(problem, q, kv->k_cache, kv->v_cache, kv, varlen, select, skip, workspace,
                  workspace_bytes, o, stream);
 }
 

@@ -5,6 +5,8 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include "cosa_internal.h"
+
 namespace cosa {
 
 typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
@@ -76,6 +78,23 @@ __device__ __forceinline__ float wave_max(float v) {
   const int a = __builtin_amdgcn_readlane(__builtin_bit_cast(int, v), 0);
   const int b = __builtin_amdgcn_readlane(__builtin_bit_cast(int, v), 16);
   return fmaxf(__builtin_bit_cast(float, a), __builtin_bit_cast(float, b));
+}
+
+// First block of the packed sequence that holds block i (0 without packing), and that sequence's
+// index: a binary search over the block offsets in the kernel arguments (uniform, scalar loads).
+__device__ __forceinline__ int pack_first(const SeqPack& sp, int i, int& seq) {
+  int lo = 0, hi = sp.n - 1;
+  if (hi < 0) {
+    seq = 0;
+    return 0;
+  }
+  while (lo < hi) {
+    const int mid = (lo + hi + 1) >> 1;
+    if (sp.cu[mid] <= i) lo = mid;
+    else hi = mid - 1;
+  }
+  seq = lo;
+  return sp.cu[lo];
 }
 
 // XCD-aware tile mapping. Workgroup ids are dealt round-robin to the 8 XCDs, so workgroup p runs on

@@ -27,12 +27,25 @@ struct KvPages {
   long long n_pages;
 };
 
+// Variable-length packing: n sequences concatenated along the token axis, sequence q owning blocks
+// [cu[q], cu[q + 1]) with cu[0] = 0 and cu[n] = nb. Query block i then only sees key blocks from its
+// own sequence's first block up to i, and the skip threshold of its sequence, tau[q] = ln(delta /
+// L_q) rounded once to float. n == 0: one unpacked sequence per batch entry. Passed by value in the
+// kernel arguments (no device memory).
+constexpr int kMaxPackedSeqs = 128;
+struct SeqPack {
+  int n;
+  int cu[kMaxPackedSeqs + 1];
+  float tau[kMaxPackedSeqs];
+};
+
 struct KapScoreArgs {
   const uint16_t* q;
   const uint16_t* k;   // contiguous K, or the paged K cache
   float* score;
   uint8_t* hrm;
   KvPages pg;
+  SeqPack pack;
 };
 
 struct KapSelectArgs {
@@ -43,6 +56,7 @@ struct KapSelectArgs {
   int mode;         // cosa_select_mode
   int order_mode;   // cosa_order_mode
   int64_t value_micro;  // budget or p in millionths
+  SeqPack pack;
 };
 
 struct AttnArgs {
@@ -59,6 +73,7 @@ struct AttnArgs {
   float tau;              // skip threshold in nats (float32)
   KvPages pg;             // k and v are the paged caches when pg.table != nullptr (OSK only)
   const uint8_t* mask;    // block mask [B, Hkv, nb, nb] (masked walk only)
+  SeqPack pack;           // packed sequences (OSK and dense walks); tau per sequence
 };
 
 // LDS bytes the proxy-scoring kernel needs for a shape (0 if the shape is outside its limits).

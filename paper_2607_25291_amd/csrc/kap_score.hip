@@ -40,6 +40,11 @@ __global__ __launch_bounds__(kScoreThreads) void kap_score_kernel(const KapParam
   const int half = lane >> 5, l32 = lane & 31;
   const int nkeys = (i + 1) * SPB;
   const int nchunks = (nkeys + 31) >> 5;
+  // Packed sequences: the candidates are the blocks F .. i of block i's own sequence.
+  int seq;
+  const int F = pack_first(P.a.pack, i, seq);
+  const int chunk0 = (F * SPB) >> 5;
+  auto cand = [&](int j) { return (unsigned)(j - F) <= (unsigned)(i - F); };
 
   // Q~^T fragments: row rt*32 + l32 = (head offset hh, sample t) -> token (i*SPB + t) * s.
   bf16x8_t qf[RT][8];
@@ -116,7 +121,7 @@ __global__ __launch_bounds__(kScoreThreads) void kap_score_kernel(const KapParam
           const float bm = fmaxf(fmaxf(acc[4 * q4], acc[4 * q4 + 1]),
                                  fmaxf(acc[4 * q4 + 2], acc[4 * q4 + 3]));
           const int j = chunk * 8 + 2 * q4 + half;
-          if (row_ok && j <= i) brow[j] = bm * P.scale;
+          if (row_ok && cand(j)) brow[j] = bm * P.scale;
         }
       } else if constexpr (SPB == 8) {
 #pragma unroll
@@ -125,7 +130,7 @@ __global__ __launch_bounds__(kScoreThreads) void kap_score_kernel(const KapParam
                            fmaxf(acc[4 * q4 + 2], acc[4 * q4 + 3]));
           bm = half_max(bm);
           const int j = chunk * 4 + q4;
-          if (row_ok && j <= i && (q4 >> 1) == half) brow[j] = bm * P.scale;
+          if (row_ok && cand(j) && (q4 >> 1) == half) brow[j] = bm * P.scale;
         }
       } else if constexpr (SPB == 16) {
 #pragma unroll
@@ -135,7 +140,7 @@ __global__ __launch_bounds__(kScoreThreads) void kap_score_kernel(const KapParam
           for (int r = 1; r < 8; ++r) bm = fmaxf(bm, acc[8 * b2 + r]);
           bm = half_max(bm);
           const int j = chunk * 2 + b2;
-          if (row_ok && j <= i && b2 == half) brow[j] = bm * P.scale;
+          if (row_ok && cand(j) && b2 == half) brow[j] = bm * P.scale;
         }
       } else {
         float bm = acc[0];
@@ -143,14 +148,14 @@ __global__ __launch_bounds__(kScoreThreads) void kap_score_kernel(const KapParam
         for (int r = 1; r < 16; ++r) bm = fmaxf(bm, acc[r]);
         bm = half_max(bm);
         const int j = chunk;
-        if (row_ok && j <= i && half == 0) brow[j] = bm * P.scale;
+        if (row_ok && cand(j) && half == 0) brow[j] = bm * P.scale;
       }
     }
   };
   // The next chunk of this wave is loaded while the current one is processed.
   bf16x8_t kcur[8], knext[8];
-  load_keys(w, kcur);
-  for (int chunk = w; chunk < nchunks; chunk += kScoreWaves) {
+  load_keys(chunk0 + w, kcur);
+  for (int chunk = chunk0 + w; chunk < nchunks; chunk += kScoreWaves) {
     load_keys(chunk + kScoreWaves, knext);
     process(chunk, kcur);
 #pragma unroll
@@ -161,7 +166,7 @@ __global__ __launch_bounds__(kScoreThreads) void kap_score_kernel(const KapParam
   // Row maxima mu (MaxNorm denominator, in the log domain).
   for (int row = w; row < P.R; row += kScoreWaves) {
     float v = -INFINITY;
-    for (int j = lane; j <= i; j += 64) v = fmaxf(v, beta[row * P.nbp + j]);
+    for (int j = F + lane; j <= i; j += 64) v = fmaxf(v, beta[row * P.nbp + j]);
     v = wave_max(v);
     if (lane == 0) mu[row] = v;
   }
@@ -169,7 +174,7 @@ __global__ __launch_bounds__(kScoreThreads) void kap_score_kernel(const KapParam
 
   float* srow = P.a.score + ((size_t)ng * P.nb + i) * P.nb;
   uint8_t* hrow = P.a.hrm + ((size_t)ng * P.nb + i) * P.nb;
-  for (int j = tid; j <= i; j += kScoreThreads) {
+  for (int j = F + tid; j <= i; j += kScoreThreads) {
     float acc = 0.f;
     int flag = 0;
     for (int row = 0; row < P.R; ++row) {

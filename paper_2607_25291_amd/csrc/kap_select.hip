@@ -1,7 +1,8 @@
 // Flag-grouped sort and stage-1 cut for gfx950 (Sec. 4.2 "Flag-grouped sorting", Eq. (mkap);
 // Algorithm A, proxy stage).
 //
-// One workgroup per (batch n, KV head g, query block i). The i+1 causal candidates become 64-bit
+// One workgroup per (batch n, KV head g, query block i). The causal candidates (j <= i, from the
+// first block of the packed sequence when several sequences share the token axis) become 64-bit
 // keys  (hrm << 63) | (float bits of score << 32) | (0xffffffff - j): scores are non-negative, so
 // their bit patterns order like the values, and comparing keys orders by HRM flag, then score, then
 // ascending block index. A bitonic sort in LDS puts them in descending key order (the HRM group
@@ -62,14 +63,18 @@ __global__ __launch_bounds__(kSelThreads) void kap_select_kernel(const SelParams
   const int i = unit % P.nb;
   const int ng = unit / P.nb;
   const int tid = threadIdx.x;
-  const int n = i + 1;
+  // Candidates: blocks F .. i (F = 0, or the first block of block i's packed sequence).
+  int seq;
+  const int F = pack_first(P.a.pack, i, seq);
+  const int n = i - F + 1;
   int n2 = 2;
   while (n2 < n) n2 <<= 1;
 
   const size_t row_off = ((size_t)ng * P.nb + i) * P.nb;
   const float* srow = P.a.score + row_off;
   const uint8_t* hrow = P.a.hrm + row_off;
-  for (int j = tid; j < n2; j += kSelThreads) keys[j] = j < n ? make_key(hrow[j], srow[j], j) : 0ull;
+  for (int t = tid; t < n2; t += kSelThreads)
+    keys[t] = t < n ? make_key(hrow[F + t], srow[F + t], F + t) : 0ull;
   __syncthreads();
   bitonic_desc(keys, n2, tid);
 

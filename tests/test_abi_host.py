@@ -15,7 +15,9 @@ EXPECTED = {"cosa_status_string", "cosa_last_error", "cosa_kap_score", "cosa_kap
             "cosa_osk_attention", "cosa_dense_attention", "cosa_prefill_workspace_bytes",
             "cosa_prefill_workspace_layout", "cosa_prefill", "cosa_kap_score_paged",
             "cosa_osk_attention_paged", "cosa_prefill_paged", "cosa_masked_attention",
-            "cosa_block_mass"}
+            "cosa_block_mass", "cosa_kap_score_varlen", "cosa_kap_select_ordered_varlen",
+            "cosa_osk_attention_varlen", "cosa_dense_attention_varlen", "cosa_prefill_varlen",
+            "cosa_prefill_paged_varlen"}
 
 
 def test_header_declares_the_abi():
@@ -126,6 +128,43 @@ def test_paged_validation():
     B.cosa_kap_score_paged(B.Problem(0, 8, 2, 1024), None, kv(v=None), None, None, stream=0)
     B.cosa_prefill_paged(B.Problem(0, 8, 2, 1024), None, kv(), sel, None, None, 0, None, stream=0)
     assert B.cosa_last_error() == ""
+
+
+def test_varlen_validation():
+    """Packing offsets must start at 0, increase strictly and end at nb (= 8 here); at most 128
+    sequences; skipping needs delta <= the shortest sequence."""
+    sel = B.select(B.SELECT_FRACTION, 0.5)
+    ws = B.cosa_prefill_workspace_bytes(GOOD)
+    bad_offsets = [[0], [1, 8], [0, 3, 3, 8], [0, 5, 2, 8], [0, 7], [0, 9], list(range(0, 130))]
+    for cu in bad_offsets:
+        vl = B.varlen(cu)
+        calls = [
+            lambda: B.cosa_kap_score_varlen(GOOD, vl, 16, 16, 16, 16, stream=0),
+            lambda: B.cosa_kap_select_ordered_varlen(GOOD, vl, 16, 16, sel, 16, 16, stream=0),
+            lambda: B.cosa_osk_attention_varlen(GOOD, vl, 16, 16, 16, 16, 16, None, 16, stream=0),
+            lambda: B.cosa_dense_attention_varlen(GOOD, vl, 16, 16, 16, 16, stream=0),
+            lambda: B.cosa_prefill_varlen(GOOD, vl, 16, 16, 16, sel, None, 16, ws, 16, stream=0),
+        ]
+        for call in calls:
+            with pytest.raises(B.CosaError) as e:
+                call()
+            assert e.value.status == B.COSA_ERR_INVALID_ARG, cu
+    for call in [lambda: B.cosa_dense_attention_varlen(GOOD, None, 16, 16, 16, 16, stream=0),
+                 lambda: B.cosa_prefill_varlen(GOOD, None, 16, 16, 16, sel, None, 16, ws, 16,
+                                               stream=0)]:
+        with pytest.raises(B.CosaError) as e:
+            call()
+        assert e.value.status == B.COSA_ERR_INVALID_ARG
+    # Delta is checked against each sequence: blocks of 128 tokens, sequences of 256 and 768 tokens
+    vl = B.varlen([0, 2, 8])
+    for delta in (257.0, 700.0):
+        with pytest.raises(B.CosaError) as e:
+            B.cosa_osk_attention_varlen(GOOD, vl, 16, 16, 16, 16, 16,
+                                        B.skip(B.SKIP_ROWMAX, delta), 16, stream=0)
+        assert e.value.status == B.COSA_ERR_INVALID_ARG
+        assert "sequence 0" in B.cosa_last_error()
+    # the same delta is accepted without packing (seq_len 1024)
+    assert B.MAX_PACKED_SEQS == 128
 
 
 def test_masked_attention_validation():
