@@ -292,6 +292,101 @@ def run_microbench(args):
     print(json.dumps({"steps": args.steps, "data": "synthetic", "records": recs}), flush=True)
 
 
+def run_varlen(args):
+    """Packed variable-length prefill: sequences of 64K, 32K, 16K and 16K tokens (32 query / 8 KV
+    heads, d = 128, b = 128, s = 16) packed into one 128K-token call, each its own causal problem
+    with its own skip threshold ln(Delta / L_q). B1 = 10 %; Delta calibrated for B2 = 5 % over the
+    pack (capped at the shortest sequence's length). Times cosa_prefill_varlen against the packed
+    dense kernel on identical inputs. One JSON object.
+    """
+    import dataclasses
+
+    import torch
+    from paper_2607_25291_amd import binding as B
+    from paper_2607_25291_amd.calibrate import delta_for_budget_packed
+    from paper_2607_25291_amd.inputs import WORKLOADS, make_inputs
+
+    dev = torch.device("cuda:0")
+    stream = torch.cuda.current_stream()
+    w = WORKLOADS["qwen3_8b_l128k"]
+    lens = [65536, 32768, 16384, 16384]
+    log(f"[varlen] generating inputs for sequences {lens}")
+    parts = [make_inputs(dataclasses.replace(w, seq_len=n, seed=s)) for s, n in enumerate(lens)]
+    q_np, k_np, v_np = (np.ascontiguousarray(np.concatenate([pt[x] for pt in parts], axis=2))
+                        for x in range(3))
+    del parts
+    cu = [0] + np.cumsum([n // w.block for n in lens]).tolist()
+    L = sum(lens)
+    nb, G = L // w.block, w.n_q_heads // w.n_kv_heads
+    p = B.Problem(w.batch, w.n_q_heads, w.n_kv_heads, L, w.head_dim, w.block, w.stride)
+    vl = B.varlen(cu)
+    up = lambda a: torch.from_numpy(a.view(np.int16)).to(dev)
+    q, k, v = up(q_np), up(k_np), up(v_np)
+    del q_np, k_np, v_np
+    o = torch.empty_like(q)
+    o_dense = torch.empty_like(q)
+    nbytes = B.cosa_prefill_workspace_bytes(p)
+    ws = torch.zeros(nbytes, dtype=torch.uint8, device=dev)
+    lay = B.cosa_prefill_workspace_layout(p)
+    cells = w.batch * w.n_kv_heads * nb * nb
+    score = ws[lay.score:lay.score + 4 * cells].view(torch.float32)
+    hrm = ws[lay.hrm:lay.hrm + cells]
+    order = ws[lay.order:lay.order + 4 * cells].view(torch.int32)
+    count = ws[lay.count:lay.count + 4 * w.batch * w.n_kv_heads * nb].view(torch.int32)
+    sel = B.select(B.SELECT_FRACTION, w.kap_budget)
+
+    # calibration (not timed): margins of every listed visit, shifted by its sequence's ln L_q
+    B.cosa_kap_score_varlen(p, vl, q, k, score, hrm)
+    B.cosa_kap_select_ordered_varlen(p, vl, score, hrm, sel, order, count)
+    margin = torch.zeros((w.batch, w.n_q_heads, nb, nb), dtype=torch.float32, device=dev)
+    B.cosa_osk_attention_varlen(p, vl, q, k, v, order, count, None, o, None, margin, None)
+    cnt_q = np.repeat(count.view(w.batch, w.n_kv_heads, nb).cpu().numpy(), G, axis=1)
+    pos = np.arange(nb)[None, None, None, :] < cnt_q[..., None]
+    len_of_block = np.repeat(np.array(lens, dtype=np.float64), [n // w.block for n in lens])
+    seq_len_of = np.broadcast_to(len_of_block[None, None, :, None], pos.shape)[pos]
+    causal = w.batch * w.n_q_heads * sum((n // w.block) * (n // w.block + 1) // 2 for n in lens)
+    listed = int(cnt_q.sum())
+    delta, n_skip, _ = delta_for_budget_packed(margin.cpu().numpy()[pos], seq_len_of, causal,
+                                               w.osk_budget)
+    del margin
+    sk = B.skip(B.SKIP_ROWMAX, delta)
+    ncomp = torch.zeros((w.batch, w.n_q_heads, nb), dtype=torch.int32, device=dev)
+    B.cosa_osk_attention_varlen(p, vl, q, k, v, order, count, sk, o, None, None, ncomp)
+    computed = int(ncomp.sum())
+    log(f"[varlen] delta {delta:.1f}: B1 {listed / causal:.4f}, B {computed / causal:.4f}")
+
+    def timed(fn, n):
+        for _ in range(max(1, args.warmup)):
+            fn()
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        for _ in range(n):
+            fn()
+        e1.record(stream)
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) / n
+
+    t_pref = timed(lambda: B.cosa_prefill_varlen(p, vl, q, k, v, sel, sk, ws, nbytes, o),
+                   args.steps)
+    t_dense = timed(lambda: B.cosa_dense_attention_varlen(p, vl, q, k, v, o_dense),
+                    max(1, args.dense_steps))
+    diff = (o.view(torch.bfloat16).float() - o_dense.view(torch.bfloat16).float()).abs()
+    rec = {"mode": "varlen", "config": {"workload": "qwen3_8b_packed_64k_32k_16k_16k",
+                                        "seq_lens": lens, "n_q_heads": w.n_q_heads,
+                                        "n_kv_heads": w.n_kv_heads, "head_dim": w.head_dim,
+                                        "block": w.block, "stride": w.stride,
+                                        "kap_budget": w.kap_budget, "osk_budget": w.osk_budget,
+                                        "delta": round(delta, 3)},
+           "steps": args.steps, "data": "synthetic",
+           "prefill_ms": round(t_pref, 4), "dense_ms": round(t_dense, 4),
+           "speedup_vs_dense": round(t_dense / t_pref, 3),
+           "realized_budget": {"stage1": round(listed / causal, 5),
+                               "overall": round(computed / causal, 5)},
+           "error_vs_dense": {"max_abs": float(diff.max()), "mean_abs": float(diff.mean())}}
+    print(json.dumps(rec), flush=True)
+
+
 def run_fidelity(args):
     """Synthetic fidelity analysis (Sec. 3.2 Property 1; Sec. 5.4 "Effect of remapping"; appendix D
     "Full remapping sweep"), with exact attention on the GPU as the ground truth.
@@ -413,6 +508,9 @@ def main():
                     help="proxy fidelity (IoU with the exact-mass oracle mask) and the remapping "
                          "skip-ratio sweep, on --fidelity-workload")
     ap.add_argument("--fidelity-workload", default="qwen3_8b_l32k")
+    ap.add_argument("--varlen", action="store_true",
+                    help="packed variable-length prefill (64K + 32K + 16K + 16K tokens in one "
+                         "call) against the packed dense kernel")
     ap.add_argument("--sweep", action="store_true",
                     help="run the budget / visiting-order sweep instead of the one-line benchmark")
     ap.add_argument("--copy-probe-mib", type=int, default=0,
@@ -431,6 +529,9 @@ def main():
         return
     if args.fidelity:
         run_fidelity(args)
+        return
+    if args.varlen:
+        run_varlen(args)
         return
 
     import torch

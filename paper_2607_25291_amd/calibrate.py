@@ -36,3 +36,30 @@ def delta_for_budget(margins: np.ndarray, n_listed: int, n_causal: int, budget: 
         tau = 0.5 * (float(d[k - 1]) + min(upper, 0.0))
     delta = seq_len * math.exp(tau)
     return delta, k, (n_listed - k) / n_causal
+
+
+def delta_for_budget_packed(margins: np.ndarray, seq_lens: np.ndarray, n_causal: int,
+                            budget: float):
+    """delta_for_budget for packed sequences, where a visit of sequence q is skipped when its margin
+    is below ln(delta / L_q) (Eq. (skip) with N = L_q). That is margin + ln L_q < ln delta, so one
+    threshold on the shifted margins serves every sequence. delta is capped at the shortest
+    length, which keeps every sequence's threshold <= 0.
+
+    margins: every listed visit's margin (nats); seq_lens: the length of the sequence each visit
+    belongs to (same shape). Returns (delta, n_skipped, realized_budget).
+    """
+    d = np.asarray(margins, dtype=np.float64).reshape(-1)
+    lens = np.asarray(seq_lens, dtype=np.float64).reshape(-1)
+    if d.shape != lens.shape:
+        raise ValueError("one sequence length per margin")
+    a = np.sort(d + np.log(lens))
+    cap = math.log(float(lens.min())) if lens.size else 0.0
+    skippable = int(np.count_nonzero(a < cap))
+    want = a.size - int(round(budget * n_causal))
+    k = min(max(want, 0), skippable)
+    if k == 0:
+        t = min(float(a[0]) - 1.0, cap) if a.size else cap
+    else:
+        upper = float(a[k]) if k < a.size else cap
+        t = 0.5 * (float(a[k - 1]) + min(upper, cap))
+    return math.exp(t), k, (a.size - k) / n_causal

@@ -9,7 +9,7 @@ import numpy as np
 import pytest
 
 from paper_2607_25291_amd import binding as B
-from paper_2607_25291_amd.calibrate import delta_for_budget
+from paper_2607_25291_amd.calibrate import delta_for_budget, delta_for_budget_packed
 
 EXPECTED = {"cosa_status_string", "cosa_last_error", "cosa_kap_score", "cosa_kap_select_ordered",
             "cosa_osk_attention", "cosa_dense_attention", "cosa_prefill_workspace_bytes",
@@ -215,3 +215,38 @@ def test_delta_for_budget_host_helper():
     # nothing to skip
     delta, k, b = delta_for_budget(m, 1000, n_causal, 0.9, 4096)
     assert k == 0 and (m < math.log(delta / 4096)).sum() == 0
+
+
+def test_delta_for_budget_packed_host_helper():
+    """Packed sequences: visit v of sequence q is skipped iff m_v < ln(delta / L_q), evaluated as the
+    kernel does (float32 delta and threshold)."""
+    rng = np.random.default_rng(1)
+    lens = np.array([4096, 1024, 16384])
+    per = [600, 200, 1200]
+    m = np.concatenate([np.concatenate([np.zeros(n // 10), -rng.exponential(2.0, n - n // 10)])
+                        for n in per])
+    seq = np.repeat(lens, per)
+    n_causal = 6000
+
+    def skipped(delta):
+        tau = np.array([np.float32(math.log(float(np.float32(delta)) / L)) for L in seq])
+        return int((m.astype(np.float32) < tau).sum())
+
+    for budget in (0.3, 0.25):  # 200 and 500 skips; at most 718 fit under delta <= 1024
+        delta, k, b = delta_for_budget_packed(m, seq, n_causal, budget)
+        assert delta <= lens.min()
+        assert skipped(delta) == k == len(m) - round(budget * n_causal)
+        assert b == (len(m) - k) / n_causal
+    # a budget below what delta <= min(L_q) allows is capped there
+    delta, k, b = delta_for_budget_packed(m, seq, n_causal, 0.01)
+    assert abs(delta - lens.min()) < 1e-6 * lens.min() or delta < lens.min()
+    assert skipped(delta) == k
+    assert k == int(((m + np.log(seq)) < math.log(lens.min())).sum())
+    # nothing to skip
+    delta, k, b = delta_for_budget_packed(m, seq, n_causal, 0.9)
+    assert k == 0 and skipped(delta) == 0
+    # one sequence reduces to the unpacked helper
+    one = m[:600]
+    d1, k1, _ = delta_for_budget_packed(one, np.full(600, 4096), 2000, 0.2)
+    d0, k0, _ = delta_for_budget(one, 600, 2000, 0.2, 4096)
+    assert k1 == k0 and abs(d1 - d0) < 1e-9 * d0
