@@ -560,6 +560,8 @@ def main():
     hrm = ws[lay.hrm:lay.hrm + cells]
     order = ws[lay.order:lay.order + 4 * cells].view(torch.int32)
     count = ws[lay.count:lay.count + 4 * w.batch * w.n_kv_heads * nb].view(torch.int32)
+    stage_bytes = B.cosa_kap_score_workspace_bytes(p)
+    keys = ws[lay.keys:lay.keys + stage_bytes]
     sel = B.select(B.SELECT_FRACTION, w.kap_budget)
     kv = None
     if args.page_size:
@@ -632,9 +634,9 @@ def main():
     evs = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(args.steps)]
     for e in evs:
         e[0].record(stream)
-        if kv is None:
-            B.cosa_kap_score(p, q, k, score, hrm)
-        else:
+        if kv is None:  # the proxy stage as cosa_prefill runs it: keys staged in the workspace
+            B.cosa_kap_score_staged(p, q, k, keys, stage_bytes, score, hrm)
+        else:           # (no standalone staged form for a paged cache: proxy read in place)
             B.cosa_kap_score_paged(p, q, kv, score, hrm)
         e[1].record(stream)
         B.cosa_kap_select_ordered(p, score, hrm, sel, order, count)

@@ -102,11 +102,12 @@ typedef struct {
 
 /* Byte offsets of the proxy tensors inside a cosa_prefill workspace (each 256-byte aligned). */
 typedef struct {
-  size_t score; /* float   [B, Hkv, nb, nb] */
-  size_t hrm;   /* uint8_t [B, Hkv, nb, nb] */
-  size_t order; /* int32_t [B, Hkv, nb, nb] */
-  size_t count; /* int32_t [B, Hkv, nb]     */
-  size_t total; /* bytes required           */
+  size_t score; /* float   [B, Hkv, nb, nb]                                         */
+  size_t hrm;   /* uint8_t [B, Hkv, nb, nb]                                         */
+  size_t order; /* int32_t [B, Hkv, nb, nb]                                         */
+  size_t count; /* int32_t [B, Hkv, nb]                                             */
+  size_t keys;  /* staged sampled keys, cosa_kap_score_workspace_bytes() (scratch)  */
+  size_t total; /* bytes required                                                   */
 } cosa_workspace_layout;
 
 /*
@@ -173,6 +174,19 @@ const char* cosa_last_error(void);
  */
 cosa_status cosa_kap_score(const cosa_problem* problem, const void* q, const void* k,
                            float* score, uint8_t* hrm, void* stream);
+
+/*
+ * cosa_kap_score with the sampled keys staged first: a copy of the L / s sampled keys of every KV
+ * head is written to the caller's workspace in the order the matrix cores consume them (32-key
+ * chunks of 8 KiB), so that the scoring kernel reads 1 KiB contiguous per load instead of 32 rows
+ * per load. Results are bit-identical to cosa_kap_score. workspace: device memory of at least
+ * cosa_kap_score_workspace_bytes() bytes, 16-byte aligned; its contents are scratch (overwritten,
+ * meaningless on return). cosa_prefill and its variants stage the keys inside their own workspace.
+ */
+size_t cosa_kap_score_workspace_bytes(const cosa_problem* problem);
+cosa_status cosa_kap_score_staged(const cosa_problem* problem, const void* q, const void* k,
+                                  void* workspace, size_t workspace_bytes, float* score,
+                                  uint8_t* hrm, void* stream);
 
 /*
  * Flag-grouped sort and stage-1 cut (Sec. 4.2, Eq. (mkap); Algorithm A, proxy stage).
@@ -243,10 +257,11 @@ cosa_status cosa_prefill_workspace_layout(const cosa_problem* problem,
                                           cosa_workspace_layout* layout);
 
 /*
- * Complete proxy-kernel workflow (Algorithm A): cosa_kap_score, cosa_kap_select_ordered and
- * cosa_osk_attention enqueued back to back on one stream, with the proxy tensors in the
- * caller-provided workspace (at least cosa_prefill_workspace_bytes(); contents on return are the
- * proxy tensors at cosa_prefill_workspace_layout() offsets). skip may be NULL.
+ * Complete proxy-kernel workflow (Algorithm A): cosa_kap_score_staged, cosa_kap_select_ordered
+ * and cosa_osk_attention enqueued back to back on one stream, with the proxy tensors and the staged
+ * keys in the caller-provided workspace (at least cosa_prefill_workspace_bytes(), 16-byte
+ * aligned; contents on return are the proxy tensors at cosa_prefill_workspace_layout() offsets).
+ * skip may be NULL.
  */
 cosa_status cosa_prefill(const cosa_problem* problem, const void* q, const void* k, const void* v,
                          const cosa_select* select, const cosa_skip* skip, void* workspace,

@@ -41,7 +41,7 @@ class CosaSkip(ctypes.Structure):
 
 class CosaWorkspaceLayout(ctypes.Structure):
     _fields_ = [("score", ctypes.c_size_t), ("hrm", ctypes.c_size_t), ("order", ctypes.c_size_t),
-                ("count", ctypes.c_size_t), ("total", ctypes.c_size_t)]
+                ("count", ctypes.c_size_t), ("keys", ctypes.c_size_t), ("total", ctypes.c_size_t)]
 
 
 class CosaPagedKv(ctypes.Structure):
@@ -136,6 +136,10 @@ def lib():
         L.cosa_prefill_paged.restype = S
         L.cosa_prefill_paged.argtypes = [P, vp, KV, ctypes.POINTER(CosaSelect),
                                          ctypes.POINTER(CosaSkip), vp, ctypes.c_size_t, vp, vp]
+        L.cosa_kap_score_workspace_bytes.restype = ctypes.c_size_t
+        L.cosa_kap_score_workspace_bytes.argtypes = [P]
+        L.cosa_kap_score_staged.restype = S
+        L.cosa_kap_score_staged.argtypes = [P, vp, vp, vp, ctypes.c_size_t, vp, vp, vp]
         VL = ctypes.POINTER(CosaVarlen)
         L.cosa_kap_score_varlen.restype = S
         L.cosa_kap_score_varlen.argtypes = [P, VL, vp, vp, vp, vp, vp]
@@ -209,6 +213,17 @@ def cosa_kap_score(problem, q, k, score, hrm, stream=None):
     p = _prob(problem)
     _check(lib().cosa_kap_score(ctypes.byref(p), _ptr(q), _ptr(k), _ptr(score), _ptr(hrm),
                                 _stream(stream)))
+
+
+def cosa_kap_score_workspace_bytes(problem) -> int:
+    p = _prob(problem)
+    return int(lib().cosa_kap_score_workspace_bytes(ctypes.byref(p)))
+
+
+def cosa_kap_score_staged(problem, q, k, workspace, workspace_bytes: int, score, hrm, stream=None):
+    p = _prob(problem)
+    _check(lib().cosa_kap_score_staged(ctypes.byref(p), _ptr(q), _ptr(k), _ptr(workspace),
+                                       workspace_bytes, _ptr(score), _ptr(hrm), _stream(stream)))
 
 
 def cosa_kap_select_ordered(problem, score, hrm, sel: CosaSelect, order, count, stream=None):

@@ -191,7 +191,8 @@ cosa_workspace_layout layout_of(const cosa::Shape& sh) {
   l.hrm = align256(l.score + cells * sizeof(float));
   l.order = align256(l.hrm + cells * sizeof(uint8_t));
   l.count = align256(l.order + cells * sizeof(int32_t));
-  l.total = align256(l.count + rows * sizeof(int32_t));
+  l.keys = align256(l.count + rows * sizeof(int32_t));
+  l.total = align256(l.keys + cosa::kap_stage_bytes(sh));
   return l;
 }
 
@@ -222,15 +223,18 @@ cosa_status prefill(const cosa_problem* problem, const void* q, const void* k, c
   if (!workspace || workspace_bytes < l.total)
     return fail(COSA_ERR_WORKSPACE, "workspace of %zu bytes at %p, need %zu", workspace_bytes,
                 workspace, l.total);
+  if (reinterpret_cast<uintptr_t>(workspace) % 16 != 0)
+    return fail(COSA_ERR_INVALID_ARG, "workspace must be 16-byte aligned");
   char* ws = static_cast<char*>(workspace);
   float* score = reinterpret_cast<float*>(ws + l.score);
   uint8_t* hrm = reinterpret_cast<uint8_t*>(ws + l.hrm);
   int32_t* order = reinterpret_cast<int32_t*>(ws + l.order);
   int32_t* count = reinterpret_cast<int32_t*>(ws + l.count);
+  uint16_t* keys = reinterpret_cast<uint16_t*>(ws + l.keys);
   const hipStream_t s = as_stream(stream);
   hipError_t e = cosa::launch_kap_score(
       sh, cosa::KapScoreArgs{static_cast<const uint16_t*>(q), static_cast<const uint16_t*>(k), score,
-                             hrm, pg, sp},
+                             hrm, pg, sp, keys},
       s);
   if (e != hipSuccess) return hip_fail(e, "kap_score launch");
   e = cosa::launch_kap_select(
@@ -274,6 +278,36 @@ cosa_status cosa_kap_score(const cosa_problem* problem, const void* q, const voi
     return fail(COSA_ERR_INVALID_ARG, "q, k, score and hrm must be non-NULL");
   cosa::KapScoreArgs a{static_cast<const uint16_t*>(q), static_cast<const uint16_t*>(k), score, hrm,
                        cosa::KvPages{}};
+  const hipError_t e = cosa::launch_kap_score(sh, a, as_stream(stream));
+  return e == hipSuccess ? ok() : hip_fail(e, "kap_score launch");
+}
+
+size_t cosa_kap_score_workspace_bytes(const cosa_problem* problem) {
+  cosa::Shape sh;
+  bool empty = false;
+  if (make_shape(problem, sh, empty) != COSA_OK) return 0;
+  return cosa::kap_stage_bytes(sh);
+}
+
+cosa_status cosa_kap_score_staged(const cosa_problem* problem, const void* q, const void* k,
+                                  void* workspace, size_t workspace_bytes, float* score,
+                                  uint8_t* hrm, void* stream) {
+  cosa::Shape sh;
+  bool empty = false;
+  cosa_status st = make_shape(problem, sh, empty);
+  if (st != COSA_OK) return st;
+  if (empty) return ok();
+  if ((st = check_proxy_limits(sh)) != COSA_OK) return st;
+  if (!q || !k || !score || !hrm)
+    return fail(COSA_ERR_INVALID_ARG, "q, k, score and hrm must be non-NULL");
+  const size_t need = cosa::kap_stage_bytes(sh);
+  if (!workspace || workspace_bytes < need)
+    return fail(COSA_ERR_WORKSPACE, "workspace of %zu bytes at %p, need %zu", workspace_bytes,
+                workspace, need);
+  if (reinterpret_cast<uintptr_t>(workspace) % 16 != 0)
+    return fail(COSA_ERR_INVALID_ARG, "workspace must be 16-byte aligned");
+  cosa::KapScoreArgs a{static_cast<const uint16_t*>(q), static_cast<const uint16_t*>(k), score, hrm,
+                       cosa::KvPages{}, cosa::SeqPack{}, static_cast<uint16_t*>(workspace)};
   const hipError_t e = cosa::launch_kap_score(sh, a, as_stream(stream));
   return e == hipSuccess ? ok() : hip_fail(e, "kap_score launch");
 }

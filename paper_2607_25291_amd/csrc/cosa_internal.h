@@ -46,6 +46,7 @@ struct KapScoreArgs {
   uint8_t* hrm;
   KvPages pg;
   SeqPack pack;
+  uint16_t* kstage;    // kap_stage_bytes() of scratch for the staged sampled keys, or nullptr
 };
 
 struct KapSelectArgs {
@@ -78,6 +79,8 @@ struct AttnArgs {
 
 // LDS bytes the proxy-scoring kernel needs for a shape (0 if the shape is outside its limits).
 size_t kap_score_lds_bytes(const Shape& sh);
+// Scratch bytes of the staged sampled keys (all L / s of every head, in MFMA operand order).
+size_t kap_stage_bytes(const Shape& sh);
 size_t kap_select_lds_bytes(const Shape& sh);
 
 hipError_t launch_kap_score(const Shape& sh, const KapScoreArgs& a, hipStream_t stream);

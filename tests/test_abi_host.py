@@ -17,7 +17,8 @@ EXPECTED = {"cosa_status_string", "cosa_last_error", "cosa_kap_score", "cosa_kap
             "cosa_osk_attention_paged", "cosa_prefill_paged", "cosa_masked_attention",
             "cosa_block_mass", "cosa_kap_score_varlen", "cosa_kap_select_ordered_varlen",
             "cosa_osk_attention_varlen", "cosa_dense_attention_varlen", "cosa_prefill_varlen",
-            "cosa_prefill_paged_varlen"}
+            "cosa_prefill_paged_varlen", "cosa_kap_score_workspace_bytes",
+            "cosa_kap_score_staged"}
 
 
 def test_header_declares_the_abi():
@@ -130,6 +131,27 @@ def test_paged_validation():
     assert B.cosa_last_error() == ""
 
 
+def test_staged_score_validation():
+    ws = B.cosa_kap_score_workspace_bytes(GOOD)
+    assert ws > 0
+    with pytest.raises(B.CosaError) as e:
+        B.cosa_kap_score_staged(GOOD, 16, 16, 256, ws - 1, 16, 16, stream=0)
+    assert e.value.status == B.COSA_ERR_WORKSPACE
+    with pytest.raises(B.CosaError) as e:
+        B.cosa_kap_score_staged(GOOD, 16, 16, None, ws, 16, 16, stream=0)
+    assert e.value.status == B.COSA_ERR_WORKSPACE
+    with pytest.raises(B.CosaError) as e:
+        B.cosa_kap_score_staged(GOOD, 16, 16, 8, ws, 16, 16, stream=0)
+    assert e.value.status == B.COSA_ERR_INVALID_ARG
+    sel = B.select(B.SELECT_ALL)
+    nbytes = B.cosa_prefill_workspace_bytes(GOOD)
+    with pytest.raises(B.CosaError) as e:
+        B.cosa_prefill(GOOD, 16, 16, 16, sel, None, 8, nbytes, 16, stream=0)
+    assert e.value.status == B.COSA_ERR_INVALID_ARG
+    B.cosa_kap_score_staged(B.Problem(0, 8, 2, 1024), None, None, None, 0, None, None, stream=0)
+    assert B.cosa_last_error() == ""
+
+
 def test_varlen_validation():
     """Packing offsets must start at 0, increase strictly and end at nb (= 8 here); at most 128
     sequences; skipping needs delta <= the shortest sequence."""
@@ -195,10 +217,14 @@ def test_workspace_layout():
         assert lay.hrm == al(4 * cells)
         assert lay.order == al(lay.hrm + cells)
         assert lay.count == al(lay.order + 4 * cells)
-        assert lay.total == al(lay.count + 4 * Bt * Hkv * nb)
+        assert lay.keys == al(lay.count + 4 * Bt * Hkv * nb)
+        # staged sampled keys: every KV head's L / s keys in 32-key chunks of 32 x 128 bf16
+        staged = Bt * Hkv * -(-(L // (b // 8)) // 32) * 32 * 128 * 2
+        assert B.cosa_kap_score_workspace_bytes(p) == staged
+        assert lay.total == al(lay.keys + staged)
         assert B.cosa_prefill_workspace_bytes(p) == lay.total
-    # 128K, 8 KV heads: 72 MiB
-    assert B.cosa_prefill_workspace_bytes(B.Problem(1, 32, 8, 131072)) == 72 * 2 ** 20 + 32 * 2 ** 10
+    # 128K, 8 KV heads: 72 MiB of proxy tensors + 16 MiB of staged keys
+    assert B.cosa_prefill_workspace_bytes(B.Problem(1, 32, 8, 131072)) == 88 * 2 ** 20 + 32 * 2 ** 10
 
 
 def test_delta_for_budget_host_helper():
