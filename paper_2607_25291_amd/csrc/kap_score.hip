@@ -1,8 +1,9 @@
 // KAP block scoring for gfx950 (Sec. 4.2 "Block ranking", Eq. (score); Algorithm A, proxy stage).
 //
 // One workgroup (8 wavefronts) per (batch n, KV head g, query block i), placed so that each XCD
-// serves as few KV heads as possible (their sampled keys then stay in that XCD's L2). Its R = G * spb sampled query
-// rows (tokens (i*spb + t) * s of the G heads of group g) stay in registers as the MFMA B operand.
+// serves as few KV heads as possible (their sampled keys then stay in that XCD's L2). Its
+// R = G * spb sampled query rows (tokens (i*spb + t) * s of the G heads of group g) stay in
+// registers as the MFMA B operand.
 // The waves stride over chunks of 32 sampled keys c < (i+1)*spb (tokens c * s), computing the
 // transposed logits K~ Q~^T with bf16 MFMA 32x32x16, applying the causal mask over sampled
 // positions (c <= r) and sm_scale, and reducing them straight into per-block maxima beta[row][j] held
@@ -253,7 +254,7 @@ __global__ __launch_bounds__(kScoreThreads) void kap_score_kernel(const KapParam
     for (int row = 0; row < P.R; ++row) {
       const float b = beta[row * P.nbp + j];
       const float mr = mu[row];
-      acc += expf(b - mr);
+      acc += __expf(b - mr);  // hardware exp2 of the scaled argument (relative error ~1e-7)
       flag |= (b == mr);
     }
     srow[j] = acc;
