@@ -309,22 +309,35 @@ void attention_kernel(const AttnParams P) {
     v_pend = (OSK || MASKED) ? listed(cur) : true;
     if (MASKED && !v_pend) return;  // a masked block: no Q K^T either
     // S^T tile t: keys 32 t + 8 (r / 4) + 4 half + r % 4 (register r) of query row qrow. The d chunk
-    // is the outer loop: the KT tiles are independent accumulation chains, and each chunk's KT
-    // fragments are read from LDS as one batch.
+    // is the outer loop: the KT tiles are independent accumulation chains. The KT fragments of
+    // chunk c + 1 are read from LDS right after the first MFMA of chunk c, so their latency hides
+    // behind that chunk's MFMAs (it is exposed when the partner wave has no P V work to fill in).
 #pragma unroll
     for (int t = 0; t < KT; ++t)
 #pragma unroll
       for (int r = 0; r < 16; ++r) s[t][r] = 0.f;
+    bf16x8_t kf[2][KT];
+#pragma unroll
+    for (int t = 0; t < KT; ++t)
+      kf[0][t] = as_bf16x8(*reinterpret_cast<const u32x4_t*>(Kb + k_rd[0] + t * 32 * 256));
+    __builtin_amdgcn_sched_group_barrier(0x100, KT, 0);
 #pragma unroll
     for (int c = 0; c < 8; ++c) {
-      bf16x8_t kf[KT];
+      if (c + 1 < 8) {
 #pragma unroll
-      for (int t = 0; t < KT; ++t)
-        kf[t] = as_bf16x8(*reinterpret_cast<const u32x4_t*>(Kb + k_rd[c] + t * 32 * 256));
+        for (int t = 0; t < KT; ++t)
+          kf[(c + 1) & 1][t] =
+              as_bf16x8(*reinterpret_cast<const u32x4_t*>(Kb + k_rd[c + 1] + t * 32 * 256));
+      }
 #pragma unroll
-      for (int t = 0; t < KT; ++t) s[t] = mfma32x32x16(kf[t], qf[c], s[t]);
-      __builtin_amdgcn_sched_group_barrier(0x100, KT, 0);  // the chunk's LDS reads ...
-      __builtin_amdgcn_sched_group_barrier(0x008, KT, 0);  // ... then its MFMAs
+      for (int t = 0; t < KT; ++t) s[t] = mfma32x32x16(kf[c & 1][t], qf[c], s[t]);
+      if (c + 1 < 8) {
+        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);       // first MFMA of chunk c,
+        __builtin_amdgcn_sched_group_barrier(0x100, KT, 0);      // the reads of chunk c + 1,
+        __builtin_amdgcn_sched_group_barrier(0x008, KT - 1, 0);  // the rest of chunk c
+      } else {
+        __builtin_amdgcn_sched_group_barrier(0x008, KT, 0);
+      }
     }
     if (j == i) {  // diagonal block: causal mask inside the tile
       // key 32 t + 8 (r / 4) + 4 half + r % 4 > query wl*32 + l32, with the lane part moved to the
