@@ -16,9 +16,12 @@
 // head start one barrier later, so phase 2m runs QK(m) of head 0 beside PV(m-1) of head 1 and phase
 // 2m+1 runs PV(m) of head 0 beside QK(m) of head 1. Waves w and w + 4 share a SIMD: while one
 // issues the Q K^T MFMAs the other runs its softmax VALU work and P V MFMAs. The waves of head 0
-// fetch K pages (page m+1 at the start of QK(m)), those of head 1 V pages (page m+1 at the start of
-// their QK(m)); a single head fetches both. A wave waits for its own copies at the end of its PV
-// half, so every copy has two phases to land before the barrier that publishes it.
+// fetch K pages (page m+1 at the end of QK(m), after its vote), those of head 1 V pages (page m+1
+// at the end of their QK(m)); a single head fetches both. Issuing a page copy stalls the issuing
+// wave for about as long as the load path takes to accept it, so it comes after the Q K^T MFMAs:
+// in a phase whose P V half computes, the copy then overlaps the partner wave's P V work instead
+// of delaying the Q K^T chain. A wave waits for its own copies at the end of its PV half, so every copy has
+// the rest of its phase and the next one to land before the barrier that publishes it.
 // With a paged KV cache (Sec. 4.3 "Physical jumping over pages"; appendix D.1) the copies gather a
 // block's rows through the page table; everything from the LDS layouts on is shared.
 //
@@ -459,11 +462,12 @@ void attention_kernel(const AttnParams P) {
     asm volatile("" ::: "memory");
   };
 
-  // Page kk, its buffers BUF: fetch page kk+1 into the other buffers, QK, barrier, PV, barrier.
+  // Page kk, its buffers BUF: QK, fetch page kk+1 into the other buffers, barrier, PV, barrier.
   auto page = [&](int kk, auto bufc) __attribute__((always_inline)) {
     constexpr int BUF = decltype(bufc)::value;
     pre = raw_entry(kk + 3);
     if constexpr (PAGED) tbl_nxt2 = table_of(nxt2);
+    qk_half(bufc);
     if (kk + 1 < cnt && (!MASKED || listed(nxt))) {
       constexpr auto NWH = std::integral_constant<int, WPH>{};
       if constexpr (HPW == 1) {
@@ -475,7 +479,6 @@ void attention_kernel(const AttnParams P) {
         copy_block(std::false_type{}, NWH, nxt, tbl_nxt, BUF ? v_lds0 : v_lds1, wl);
       }
     }
-    qk_half(bufc);
     end_phase(false);
     pv_half(kk, bufc);
     end_phase(true);
