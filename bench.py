@@ -8,7 +8,8 @@
 A step is one pass of the whole hot path, cosa_prefill (proxy scoring, ordered selection, ordered-
 skipping attention) over one attention layer of synthetic bf16 inputs that are already resident in
 HBM. The skip scale Delta is calibrated once, before timing, so that the in-kernel skip reaches the
-workload's overall budget. Prints one JSON line (see the "value"/"roofline"/"cpu_baseline" keys).
+workload's overall budget. Prints one JSON line (see the "value"/"roofline"/"cpu_baseline" keys;
+"mfma_ceiling" is the vendor library's bf16 GEMM rate measured in the same run, as context).
 """
 from __future__ import annotations
 
@@ -73,6 +74,28 @@ def traffic_from_profile(kernel_tag: str, src: str):
     if rec.get("source_sha256_16") != source_hash(src):
         return None
     return rec.get("bytes_per_launch")
+
+
+def gemm_ceiling(n: int = 16384, reps: int = 5) -> float:
+    """TFLOP/s of the vendor library's bf16 GEMM (torch.matmul, hipBLASLt) on n x n x n random
+    operands: the MFMA throughput this GPU actually sustains under power and clock limits, measured
+    in the same run as context for the roofline fraction (which stays against the 2.5 PFLOP/s
+    nominal peak). A calibration reference only; no step of the attention path uses it."""
+    import torch
+    a = torch.randn(n, n, device="cuda", dtype=torch.bfloat16)
+    b = torch.randn(n, n, device="cuda", dtype=torch.bfloat16)
+    c = a @ b
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(reps):
+        c = a @ b
+    e1.record()
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / reps
+    del a, b, c
+    torch.cuda.empty_cache()
+    return 2.0 * n ** 3 / (ms * 1e-3) / 1e12
 
 
 def cpu_baseline(w, q, k, v, gpu_count, gpu_ncomp, delta, budget_s: float = 15.0):
@@ -498,6 +521,8 @@ def main():
     ap.add_argument("--workload", default="qwen3_8b_l128k")
     ap.add_argument("--dense-steps", type=int, default=3)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-gemm-ceiling", action="store_true",
+                    help="skip the library bf16 GEMM reference measurement")
     ap.add_argument("--page-size", type=int, default=0,
                     help="time cosa_prefill_paged on a paged KV cache with this page size "
                          "(pages placed by a random permutation); 0: contiguous K/V")
@@ -679,6 +704,14 @@ def main():
                             w.head_dim)
     traffic = None if args.page_size else traffic_from_profile("osk_attention", "attention.hip")
 
+    ceiling = None
+    if not args.no_gemm_ceiling:
+        g_tflops = gemm_ceiling()
+        log(f"[bench] library bf16 GEMM 16384^3: {g_tflops:.0f} TFLOP/s")
+        ceiling = {"what": "torch.matmul bf16 16384x16384x16384 (hipBLASLt), same run",
+                   "tflops": round(g_tflops, 1), "frac_of_peak": round(g_tflops / PEAK_BF16_TFLOPS, 4),
+                   "osk_frac_of_ceiling": round(osk_tflops / g_tflops, 4)}
+
     cpu = None
     if not args.no_cpu_baseline:
         log("[bench] timing the oracle on a sample (cpu_baseline)")
@@ -719,6 +752,7 @@ def main():
                                "mfma_tflops": round(kf / (t_score * 1e-3) / 1e12, 1),
                                "mfma_frac": round(kf / (t_score * 1e-3) / 1e12 / PEAK_BF16_TFLOPS,
                                                   4)},
+        "mfma_ceiling": ceiling,
         "cpu_baseline": cpu,
     }
     print(json.dumps(out), flush=True)
