@@ -587,6 +587,8 @@ def main():
     count = ws[lay.count:lay.count + 4 * w.batch * w.n_kv_heads * nb].view(torch.int32)
     stage_bytes = B.cosa_kap_score_workspace_bytes(p)
     keys = ws[lay.keys:lay.keys + stage_bytes]
+    queue_bytes = B.cosa_osk_attention_queue_bytes()
+    queue = ws[lay.queue:lay.queue + queue_bytes]
     sel = B.select(B.SELECT_FRACTION, w.kap_budget)
     kv = None
     if args.page_size:
@@ -666,8 +668,8 @@ def main():
         e[1].record(stream)
         B.cosa_kap_select_ordered(p, score, hrm, sel, order, count)
         e[2].record(stream)
-        if kv is None:
-            B.cosa_osk_attention(p, q, k, v, order, count, sk, o, None, None, None)
+        if kv is None:  # the walk as cosa_prefill runs it: persistent grid fed by work queues
+            B.cosa_osk_attention_queued(p, q, k, v, order, count, sk, o, queue, queue_bytes)
         else:
             B.cosa_osk_attention_paged(p, q, kv, order, count, sk, o, None, None, None)
         e[3].record(stream)

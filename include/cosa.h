@@ -107,6 +107,7 @@ typedef struct {
   size_t order; /* int32_t [B, Hkv, nb, nb]                                         */
   size_t count; /* int32_t [B, Hkv, nb]                                             */
   size_t keys;  /* staged sampled keys, cosa_kap_score_workspace_bytes() (scratch)  */
+  size_t queue; /* OSK work-queue counters, cosa_osk_attention_queue_bytes() (scratch) */
   size_t total; /* bytes required                                                   */
 } cosa_workspace_layout;
 
@@ -215,6 +216,22 @@ cosa_status cosa_osk_attention(const cosa_problem* problem, const void* q, const
                                const void* v, const int32_t* order, const int32_t* count,
                                const cosa_skip* skip, void* o, uint8_t* visit_log,
                                float* margin_log, int32_t* n_computed, void* stream);
+
+/*
+ * cosa_osk_attention as cosa_prefill runs it: a persistent grid of one workgroup per compute unit
+ * that takes (query block, head pair) tiles from eight work queues, one per XCD, heaviest query
+ * blocks first; a workgroup drains its own XCD's queue, then the others. Same arguments, results
+ * and logs as cosa_osk_attention, bit for bit. queue: device memory of at least
+ * cosa_osk_attention_queue_bytes() bytes, 4-byte aligned, owned by the caller; its contents are
+ * scratch (reset by the call on the stream, meaningless on return), so calls that may run at the
+ * same time need distinct queue buffers. Returns COSA_ERR_WORKSPACE if queue is NULL or too small.
+ */
+size_t cosa_osk_attention_queue_bytes(void);
+cosa_status cosa_osk_attention_queued(const cosa_problem* problem, const void* q, const void* k,
+                                      const void* v, const int32_t* order, const int32_t* count,
+                                      const cosa_skip* skip, void* o, uint8_t* visit_log,
+                                      float* margin_log, int32_t* n_computed, void* queue,
+                                      size_t queue_bytes, void* stream);
 
 /*
  * Dense causal flash attention (Sec. 3.1): every key block j <= i in ascending order, same tile

@@ -41,7 +41,8 @@ class CosaSkip(ctypes.Structure):
 
 class CosaWorkspaceLayout(ctypes.Structure):
     _fields_ = [("score", ctypes.c_size_t), ("hrm", ctypes.c_size_t), ("order", ctypes.c_size_t),
-                ("count", ctypes.c_size_t), ("keys", ctypes.c_size_t), ("total", ctypes.c_size_t)]
+                ("count", ctypes.c_size_t), ("keys", ctypes.c_size_t), ("queue", ctypes.c_size_t),
+                ("total", ctypes.c_size_t)]
 
 
 class CosaPagedKv(ctypes.Structure):
@@ -114,6 +115,11 @@ def lib():
         L.cosa_osk_attention.restype = S
         L.cosa_osk_attention.argtypes = [P, vp, vp, vp, vp, vp, ctypes.POINTER(CosaSkip), vp, vp,
                                          vp, vp, vp]
+        L.cosa_osk_attention_queue_bytes.restype = ctypes.c_size_t
+        L.cosa_osk_attention_queue_bytes.argtypes = []
+        L.cosa_osk_attention_queued.restype = S
+        L.cosa_osk_attention_queued.argtypes = [P, vp, vp, vp, vp, vp, ctypes.POINTER(CosaSkip), vp,
+                                                vp, vp, vp, vp, ctypes.c_size_t, vp]
         L.cosa_dense_attention.restype = S
         L.cosa_dense_attention.argtypes = [P, vp, vp, vp, vp, vp]
         L.cosa_prefill_workspace_bytes.restype = ctypes.c_size_t
@@ -239,6 +245,21 @@ def cosa_osk_attention(problem, q, k, v, order, count, sk: Optional[CosaSkip], o
     _check(lib().cosa_osk_attention(ctypes.byref(p), _ptr(q), _ptr(k), _ptr(v), _ptr(order),
                                     _ptr(count), skp, _ptr(o), _ptr(visit_log), _ptr(margin_log),
                                     _ptr(n_computed), _stream(stream)))
+
+
+def cosa_osk_attention_queue_bytes() -> int:
+    return int(lib().cosa_osk_attention_queue_bytes())
+
+
+def cosa_osk_attention_queued(problem, q, k, v, order, count, sk: Optional[CosaSkip], o, queue,
+                              queue_bytes: int, visit_log=None, margin_log=None, n_computed=None,
+                              stream=None):
+    p = _prob(problem)
+    skp = ctypes.byref(sk) if sk is not None else None
+    _check(lib().cosa_osk_attention_queued(ctypes.byref(p), _ptr(q), _ptr(k), _ptr(v), _ptr(order),
+                                           _ptr(count), skp, _ptr(o), _ptr(visit_log),
+                                           _ptr(margin_log), _ptr(n_computed), _ptr(queue),
+                                           queue_bytes, _stream(stream)))
 
 
 def cosa_dense_attention(problem, q, k, v, o, stream=None):

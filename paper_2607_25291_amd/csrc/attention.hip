@@ -140,7 +140,12 @@ constexpr int kWalkDense = 0;  // j = 0 .. i ascending, every block computed
 constexpr int kWalkList = 1;   // OSK: the KAP list in list order, rowmax skip vote
 constexpr int kWalkMask = 2;   // j = 0 .. i ascending, blocks whose mask byte is 0 skipped in-loop
 
-template <int BLOCK, int HPW, int WALK, bool PAGED>
+// Zeroes the work-queue counters of a persistent OSK launch (one per XCD, 128 bytes apart).
+__global__ void queue_reset(uint32_t* queue) {
+  if (threadIdx.x < kNumXcd) queue[threadIdx.x * 32] = 0u;
+}
+
+template <int BLOCK, int HPW, int WALK, bool PAGED, bool PERSIST>
 __global__ __attribute__((amdgpu_flat_work_group_size(TileCfg<BLOCK, HPW>::kThreads,
                                                       TileCfg<BLOCK, HPW>::kThreads)))
 __attribute__((amdgpu_waves_per_eu(TileCfg<BLOCK, HPW>::kWavesPerEu,
@@ -159,9 +164,55 @@ void attention_kernel(const AttnParams P) {
   __shared__ __attribute__((aligned(1024))) char k_lds0[PAGE];
   __shared__ __attribute__((aligned(1024))) char k_lds1[PAGE];
   __shared__ float vote[2][Cfg::kWaves];
+  __shared__ int tile_slot;
 
+  // Persistent grid (OSK with a work queue): one workgroup per CU takes tiles until none are left.
+  // Slot p is the tile the hardware would run as workgroup p; queue x hands out the slots
+  // p = x + 8 k, which the hardware would deal to XCD x, heaviest first. A workgroup starts on its
+  // own XCD's queue and moves on to the next one when that is empty, so every tile is taken exactly
+  // once and every workgroup leaves once all eight queues are empty. Thread 0 claims the next slot
+  // during the last page of the current tile, which hides the atomic's latency without holding a
+  // slot for long, and broadcasts it through LDS.
+  const int n_slots = (P.n_units + kNumXcd - 1) / kNumXcd * kNumXcd * (P.G / HPW);
+  int qx = PERSIST ? (int)(__builtin_amdgcn_s_getreg(0xF814) & (kNumXcd - 1)) : 0;  // XCC_ID
+  int qtried = 0;
+  unsigned k_next = 0u;
+  bool have_next = false;
+  auto claim = [&]() -> int {
+    while (qtried < kNumXcd) {
+      const int p = qx + kNumXcd * (int)atomicAdd(&P.a.queue[qx * 32], 1u);
+      if (p < n_slots) return p;
+      qx = (qx + 1) & (kNumXcd - 1);
+      ++qtried;
+    }
+    return -1;
+  };
+  for (;;) {
   int unit, pair;
-  if (!map_tile(blockIdx.x, P.G / HPW, P.n_units, unit, pair)) return;
+  if constexpr (PERSIST) {
+    if (threadIdx.x == 0) {
+      int p = -1;
+      if (have_next) {
+        p = qx + kNumXcd * (int)k_next;
+        if (p >= n_slots) {
+          qx = (qx + 1) & (kNumXcd - 1);
+          ++qtried;
+          p = claim();
+        }
+      } else {
+        p = claim();
+      }
+      have_next = false;
+      tile_slot = p;
+    }
+    __syncthreads();
+    const int ps = __builtin_amdgcn_readfirstlane(tile_slot);
+    __syncthreads();
+    if (ps < 0) return;
+    if (!map_tile(ps, P.G / HPW, P.n_units, unit, pair)) continue;
+  } else {
+    if (!map_tile(blockIdx.x, P.G / HPW, P.n_units, unit, pair)) return;
+  }
   const int i = P.nb - 1 - (unit % P.nb);  // heaviest query blocks first
   const int ng = unit / P.nb;              // n * Hkv + g
   const int g = ng % P.Hkv, n = ng / P.Hkv;
@@ -465,6 +516,12 @@ void attention_kernel(const AttnParams P) {
   // Page kk, its buffers BUF: QK, fetch page kk+1 into the other buffers, barrier, PV, barrier.
   auto page = [&](int kk, auto bufc) __attribute__((always_inline)) {
     constexpr int BUF = decltype(bufc)::value;
+    if constexpr (PERSIST) {
+      if (kk == cnt - 1 && threadIdx.x == 0 && qtried < kNumXcd) {
+        k_next = atomicAdd(&P.a.queue[qx * 32], 1u);
+        have_next = true;
+      }
+    }
     pre = raw_entry(kk + 3);
     if constexpr (PAGED) tbl_nxt2 = table_of(nxt2);
     qk_half(bufc);
@@ -517,14 +574,30 @@ void attention_kernel(const AttnParams P) {
     if (wl == 0 && lane == 0 && P.a.n_computed)
       P.a.n_computed[(size_t)(n * P.Hq + h) * P.nb + i] = ncomp;
   }
+  if constexpr (!PERSIST) break;
+  }  // tiles of a persistent workgroup
 }
 
 template <int BLOCK, int HPW, int WALK, bool PAGED>
 void launch_t(const AttnParams& P, int G, hipStream_t stream) {
   using Cfg = TileCfg<BLOCK, HPW>;
   const int slots = (P.n_units + kNumXcd - 1) / kNumXcd * kNumXcd * (G / HPW);
-  hipLaunchKernelGGL((attention_kernel<BLOCK, HPW, WALK, PAGED>), dim3(slots), dim3(Cfg::kThreads),
-                     0, stream, P);
+  if constexpr (WALK == kWalkList) {
+    if (P.a.queue != nullptr) {
+      // One workgroup per CU (the LDS footprint admits one), fed by the work queues.
+      int dev = 0, cus = 0;
+      if (hipGetDevice(&dev) != hipSuccess ||
+          hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
+          cus < 1)
+        cus = 256;
+      hipLaunchKernelGGL(queue_reset, dim3(1), dim3(64), 0, stream, P.a.queue);
+      hipLaunchKernelGGL((attention_kernel<BLOCK, HPW, WALK, PAGED, true>),
+                         dim3(cus < slots ? cus : slots), dim3(Cfg::kThreads), 0, stream, P);
+      return;
+    }
+  }
+  hipLaunchKernelGGL((attention_kernel<BLOCK, HPW, WALK, PAGED, false>), dim3(slots),
+                     dim3(Cfg::kThreads), 0, stream, P);
 }
 
 template <int WALK, bool PAGED>

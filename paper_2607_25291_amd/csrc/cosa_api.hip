@@ -192,7 +192,8 @@ cosa_workspace_layout layout_of(const cosa::Shape& sh) {
   l.order = align256(l.hrm + cells * sizeof(uint8_t));
   l.count = align256(l.order + cells * sizeof(int32_t));
   l.keys = align256(l.count + rows * sizeof(int32_t));
-  l.total = align256(l.keys + cosa::kap_stage_bytes(sh));
+  l.queue = align256(l.keys + cosa::kap_stage_bytes(sh));
+  l.total = align256(l.queue + cosa::kOskQueueBytes);
   return l;
 }
 
@@ -231,6 +232,7 @@ cosa_status prefill(const cosa_problem* problem, const void* q, const void* k, c
   int32_t* order = reinterpret_cast<int32_t*>(ws + l.order);
   int32_t* count = reinterpret_cast<int32_t*>(ws + l.count);
   uint16_t* keys = reinterpret_cast<uint16_t*>(ws + l.keys);
+  uint32_t* queue = reinterpret_cast<uint32_t*>(ws + l.queue);
   const hipStream_t s = as_stream(stream);
   hipError_t e = cosa::launch_kap_score(
       sh, cosa::KapScoreArgs{static_cast<const uint16_t*>(q), static_cast<const uint16_t*>(k), score,
@@ -244,7 +246,7 @@ cosa_status prefill(const cosa_problem* problem, const void* q, const void* k, c
   if (e != hipSuccess) return hip_fail(e, "kap_select launch");
   cosa::AttnArgs a{static_cast<const uint16_t*>(q), static_cast<const uint16_t*>(k),
                    static_cast<const uint16_t*>(v), static_cast<uint16_t*>(o), order, count,
-                   nullptr, nullptr, nullptr, on, tau, pg, nullptr, sp};
+                   nullptr, nullptr, nullptr, on, tau, pg, nullptr, sp, queue};
   e = cosa::launch_osk_attention(sh, a, s);
   return e == hipSuccess ? ok() : hip_fail(e, "osk_attention launch");
 }
@@ -364,6 +366,36 @@ cosa_status cosa_osk_attention(const cosa_problem* problem, const void* q, const
   cosa::AttnArgs a{static_cast<const uint16_t*>(q), static_cast<const uint16_t*>(k),
                    static_cast<const uint16_t*>(v), static_cast<uint16_t*>(o), order, count,
                    visit_log, margin_log, n_computed, on, tau, cosa::KvPages{}};
+  const hipError_t e = cosa::launch_osk_attention(sh, a, as_stream(stream));
+  return e == hipSuccess ? ok() : hip_fail(e, "osk_attention launch");
+}
+
+size_t cosa_osk_attention_queue_bytes(void) { return cosa::kOskQueueBytes; }
+
+cosa_status cosa_osk_attention_queued(const cosa_problem* problem, const void* q, const void* k,
+                                      const void* v, const int32_t* order, const int32_t* count,
+                                      const cosa_skip* skip, void* o, uint8_t* visit_log,
+                                      float* margin_log, int32_t* n_computed, void* queue,
+                                      size_t queue_bytes, void* stream) {
+  cosa::Shape sh;
+  bool empty = false;
+  cosa_status st = make_shape(problem, sh, empty);
+  if (st != COSA_OK) return st;
+  int on = 0;
+  float tau = 0.f;
+  if ((st = check_skip(skip, sh, on, tau)) != COSA_OK) return st;
+  if (empty) return ok();
+  if (!q || !k || !v || !order || !count || !o)
+    return fail(COSA_ERR_INVALID_ARG, "q, k, v, order, count and o must be non-NULL");
+  if (!queue || queue_bytes < cosa::kOskQueueBytes)
+    return fail(COSA_ERR_WORKSPACE, "queue of %zu bytes at %p, need %zu", queue_bytes, queue,
+                cosa::kOskQueueBytes);
+  if (reinterpret_cast<uintptr_t>(queue) % 4 != 0)
+    return fail(COSA_ERR_INVALID_ARG, "queue must be 4-byte aligned");
+  cosa::AttnArgs a{static_cast<const uint16_t*>(q), static_cast<const uint16_t*>(k),
+                   static_cast<const uint16_t*>(v), static_cast<uint16_t*>(o), order, count,
+                   visit_log, margin_log, n_computed, on, tau, cosa::KvPages{}, nullptr,
+                   cosa::SeqPack{}, static_cast<uint32_t*>(queue)};
   const hipError_t e = cosa::launch_osk_attention(sh, a, as_stream(stream));
   return e == hipSuccess ? ok() : hip_fail(e, "osk_attention launch");
 }

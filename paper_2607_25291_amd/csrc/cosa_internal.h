@@ -75,7 +75,11 @@ struct AttnArgs {
   KvPages pg;             // k and v are the paged caches when pg.table != nullptr (OSK only)
   const uint8_t* mask;    // block mask [B, Hkv, nb, nb] (masked walk only)
   SeqPack pack;           // packed sequences (OSK and dense walks); tau per sequence
+  uint32_t* queue;        // OSK: kOskQueueBytes of work-queue counters (persistent grid), or nullptr
 };
+
+// Work-queue counters of the persistent OSK grid: one 32-bit counter per XCD, 128 bytes apart.
+constexpr size_t kOskQueueBytes = kNumXcd * 128;
 
 // LDS bytes the proxy-scoring kernel needs for a shape (0 if the shape is outside its limits).
 size_t kap_score_lds_bytes(const Shape& sh);

@@ -18,7 +18,7 @@ EXPECTED = {"cosa_status_string", "cosa_last_error", "cosa_kap_score", "cosa_kap
             "cosa_block_mass", "cosa_kap_score_varlen", "cosa_kap_select_ordered_varlen",
             "cosa_osk_attention_varlen", "cosa_dense_attention_varlen", "cosa_prefill_varlen",
             "cosa_prefill_paged_varlen", "cosa_kap_score_workspace_bytes",
-            "cosa_kap_score_staged"}
+            "cosa_kap_score_staged", "cosa_osk_attention_queue_bytes", "cosa_osk_attention_queued"}
 
 
 def test_header_declares_the_abi():
@@ -103,6 +103,27 @@ def test_argument_validation():
         B.cosa_prefill(GOOD, 16, 16, 16, B.select(B.SELECT_FRACTION, 0.5), None, None, ws, 16,
                        stream=0)
     assert e.value.status == B.COSA_ERR_WORKSPACE
+
+
+def test_queued_osk_validation():
+    """The queued OSK checks what cosa_osk_attention checks, plus its queue buffer."""
+    qb = B.cosa_osk_attention_queue_bytes()
+    for queue, nbytes, status in [(None, qb, B.COSA_ERR_WORKSPACE), (256, qb - 1, B.COSA_ERR_WORKSPACE),
+                                  (258, qb, B.COSA_ERR_INVALID_ARG)]:
+        with pytest.raises(B.CosaError) as e:
+            B.cosa_osk_attention_queued(GOOD, 16, 16, 16, 16, 16, None, 16, queue, nbytes, stream=0)
+        assert e.value.status == status
+    with pytest.raises(B.CosaError) as e:
+        B.cosa_osk_attention_queued(GOOD, 16, 16, 16, 16, 16, B.skip(B.SKIP_ROWMAX, 0.0), 16, 256,
+                                    qb, stream=0)
+    assert e.value.status == B.COSA_ERR_INVALID_ARG
+    with pytest.raises(B.CosaError) as e:
+        B.cosa_osk_attention_queued(GOOD, 16, 16, 16, None, 16, None, 16, 256, qb, stream=0)
+    assert e.value.status == B.COSA_ERR_INVALID_ARG
+    # an empty problem launches nothing, whatever the pointers
+    B.cosa_osk_attention_queued(B.Problem(0, 8, 2, 1024), None, None, None, None, None, None, None,
+                                None, 0, stream=0)
+    assert B.cosa_last_error() == ""
 
 
 def test_paged_validation():
@@ -221,10 +242,14 @@ def test_workspace_layout():
         # staged sampled keys: every KV head's L / s keys in 32-key chunks of 32 x 128 bf16
         staged = Bt * Hkv * -(-(L // (b // 8)) // 32) * 32 * 128 * 2
         assert B.cosa_kap_score_workspace_bytes(p) == staged
-        assert lay.total == al(lay.keys + staged)
+        # the OSK work-queue counters (one per XCD, 128 bytes apart) close the workspace
+        assert lay.queue == al(lay.keys + staged)
+        assert B.cosa_osk_attention_queue_bytes() == 8 * 128
+        assert lay.total == al(lay.queue + 8 * 128)
         assert B.cosa_prefill_workspace_bytes(p) == lay.total
-    # 128K, 8 KV heads: 72 MiB of proxy tensors + 16 MiB of staged keys
-    assert B.cosa_prefill_workspace_bytes(B.Problem(1, 32, 8, 131072)) == 88 * 2 ** 20 + 32 * 2 ** 10
+    # 128K, 8 KV heads: 72 MiB of proxy tensors + 16 MiB of staged keys + 1 KiB of queue counters
+    assert (B.cosa_prefill_workspace_bytes(B.Problem(1, 32, 8, 131072))
+            == 88 * 2 ** 20 + 32 * 2 ** 10 + 1024)
 
 
 def test_delta_for_budget_host_helper():
