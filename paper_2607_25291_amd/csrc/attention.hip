@@ -43,6 +43,14 @@ namespace cosa {
 namespace {
 
 typedef short s16x4_t __attribute__((ext_vector_type(4)));
+
+// A wave-uniform read of data this kernel never writes (the count and first list entries in a
+// tile's prologue), through the constant address space: a scalar load, counted apart from the
+// vector memory operations (the Q fragments) already in flight. Inside the page loop the list is
+// read with vector loads instead: an outstanding scalar load would make every LDS wait a full one.
+__device__ __forceinline__ int32_t ld_uniform(const int32_t* p) {
+  return *(const __attribute__((address_space(4))) int32_t*)(size_t)p;
+}
 #define COSA_LDS(p) ((__attribute__((address_space(3))) void*)(p))
 
 // s_waitcnt immediates (vmcnt in bits 3:0 and 15:14, expcnt 6:4, lgkmcnt 11:8): wait for vector
@@ -230,6 +238,15 @@ void attention_kernel(const AttnParams P) {
   const __amdgpu_buffer_rsrc_t vrs = __builtin_amdgcn_make_buffer_rsrc(
       (void*)(P.a.v + kv_off), (short)0, P.L * kHeadDim * 2, 0x00020000);
 
+  // Q^T as the MFMA B operand: lane owns query row qrow, 8 chunks of 16 d (8 per lane half). Loaded
+  // first: it does not depend on the list, so its latency overlaps the list reads below.
+  bf16x8_t qf[8];
+  {
+    const uint16_t* qp = P.a.q + qo_off + (size_t)qrow * kHeadDim + 8 * half;
+#pragma unroll
+    for (int c = 0; c < 8; ++c) qf[c] = as_bf16x8(ldg16(qp + 16 * c));
+  }
+
   // Packed sequences: block i only sees the blocks F .. i of its own sequence, whose skip
   // threshold is its own (F = 0 and the call's threshold without packing; the masked walk is
   // never packed).
@@ -240,7 +257,7 @@ void attention_kernel(const AttnParams P) {
   const int32_t* lst = nullptr;
   const uint8_t* mrow = nullptr;
   if constexpr (OSK) {
-    cnt = P.a.count[(size_t)ng * P.nb + i];
+    cnt = ld_uniform(P.a.count + (size_t)ng * P.nb + i);
     cnt = cnt < P.nb ? cnt : P.nb;
     lst = P.a.order + ((size_t)ng * P.nb + i) * P.nb;
   } else {
@@ -289,9 +306,13 @@ void attention_kernel(const AttnParams P) {
   };
 
   // Prologue: K and V of page 0.
-  const int raw0 = __builtin_amdgcn_readfirstlane(raw_entry(0));
-  const int raw1 = __builtin_amdgcn_readfirstlane(raw_entry(1));
-  const int raw2 = __builtin_amdgcn_readfirstlane(raw_entry(2));
+  auto first_entry = [&](int kk) -> int {
+    if constexpr (OSK) return kk < cnt ? ld_uniform(lst + kk) : 0;
+    else return raw_entry(kk);
+  };
+  const int raw0 = __builtin_amdgcn_readfirstlane(first_entry(0));
+  const int raw1 = __builtin_amdgcn_readfirstlane(first_entry(1));
+  const int raw2 = __builtin_amdgcn_readfirstlane(first_entry(2));
   int tbl_nxt = 0;
   if constexpr (PAGED) {
     const int tbl0 = table_of(raw0);
@@ -309,13 +330,6 @@ void attention_kernel(const AttnParams P) {
     }
   }
 
-  // Q^T as the MFMA B operand: lane owns query row qrow, 8 chunks of 16 d (8 per lane half).
-  bf16x8_t qf[8];
-  {
-    const uint16_t* qp = P.a.q + qo_off + (size_t)qrow * kHeadDim + 8 * half;
-#pragma unroll
-    for (int c = 0; c < 8; ++c) qf[c] = as_bf16x8(ldg16(qp + 16 * c));
-  }
   // O^T accumulators: tile dt holds d = 32 dt + 8 (r / 4) + 4 half + r % 4 of row qrow.
   f32x16_t o[4];
 #pragma unroll
