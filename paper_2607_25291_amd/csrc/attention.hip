@@ -458,6 +458,9 @@ void attention_kernel(const AttnParams P) {
     }
     // A skip implies m_loc < m in every row, so the running max is unchanged either way.
     if (!skip) {
+      // A computing P V half is the critical path of its phase (softmax VALU, then its MFMAs,
+      // beside the partner's Q K^T): its wave issues first, the partner fills the gaps.
+      __builtin_amdgcn_s_setprio(1);
       const float alpha = __builtin_amdgcn_exp2f((m - mnew) * P.scale_log2);
       m = mnew;
       const float mb = mnew * P.scale_log2;
@@ -512,6 +515,7 @@ void attention_kernel(const AttnParams P) {
         __builtin_amdgcn_sched_group_barrier(0x008, 4, 0);  // ... then its MFMAs
       }
       ++ncomp;
+      __builtin_amdgcn_s_setprio(0);
     }
   };
 
