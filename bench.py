@@ -64,14 +64,15 @@ def kap_score_work(B, Hq, Hkv, nb, b, s, d):
     return flops, bytes_
 
 
-def traffic_from_profile(kernel_tag: str, src: str):
-    """HBM bytes per launch from a committed rocprofv3 counter summary, if it matches the source."""
+def traffic_from_profile(kernel_tag: str, src: str, workload: str):
+    """HBM bytes per launch from a committed rocprofv3 counter summary, if it was taken on this
+    workload and matches the current source."""
     path = os.path.join(ROOT, "profiles", f"{kernel_tag}_traffic.json")
     if not os.path.exists(path):
         return None
     with open(path) as f:
         rec = json.load(f)
-    if rec.get("source_sha256_16") != source_hash(src):
+    if rec.get("source_sha256_16") != source_hash(src) or rec.get("workload") != workload:
         return None
     return rec.get("bytes_per_launch")
 
@@ -704,7 +705,8 @@ def main():
     dense_tflops = f_dense / (t_dense * 1e-3) / 1e12 if t_dense else None
     kf, kb = kap_score_work(w.batch, w.n_q_heads, w.n_kv_heads, nb, w.block, w.stride,
                             w.head_dim)
-    traffic = None if args.page_size else traffic_from_profile("osk_attention", "attention.hip")
+    traffic = (None if args.page_size
+               else traffic_from_profile("osk_attention", "attention.hip", w.name))
 
     ceiling = None
     if not args.no_gemm_ceiling:
