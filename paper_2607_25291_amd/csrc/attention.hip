@@ -20,8 +20,12 @@
 // at the end of their QK(m)); a single head fetches both. Issuing a page copy stalls the issuing
 // wave for about as long as the load path takes to accept it, so it comes after the Q K^T MFMAs:
 // in a phase whose P V half computes, the copy then overlaps the partner wave's P V work instead
-// of delaying the Q K^T chain. A wave waits for its own copies at the end of its PV half, so every copy has
-// the rest of its phase and the next one to land before the barrier that publishes it.
+// of delaying the Q K^T chain. A wave waits for its own copies at the end of its PV half, so every
+// copy has the rest of its phase and the next one to land before the barrier that publishes it.
+//
+// The grid is either one workgroup per tile (query block, head pair) or, when the caller supplies
+// work-queue counters, persistent: one workgroup per CU takes tiles from per-XCD queues in the
+// order the hardware would run them (see the tile loop below).
 // With a paged KV cache (Sec. 4.3 "Physical jumping over pages"; appendix D.1) the copies gather a
 // block's rows through the page table; everything from the LDS layouts on is shared.
 //
