@@ -437,8 +437,16 @@ void attention_kernel(const AttnParams P) {
     mloc = half_max(mloc);
     mnew = v_pend ? fmaxf(m, mloc) : m;
     if constexpr (OSK) {
-      // Eq. (skip): each head's b-row tile votes with its largest (m_loc - m), in nats.
-      const float marg = wave_max((mloc - mnew) * P.scale);
+      // Eq. (skip): each head's b-row tile votes with its largest (m_loc - m), in nats. Unless
+      // that margin is logged, only its comparison with tau matters: the tile is skipped exactly
+      // when every row's margin is below tau, so a ballot replaces the cross-lane maximum and the
+      // wave votes 0 (some row reaches tau; tau <= 0) or -inf (none does).
+      const float d = (mloc - mnew) * P.scale;
+      float marg;
+      if (P.a.margin_log)
+        marg = wave_max(d);
+      else
+        marg = __ballot(d >= tau) ? 0.f : -INFINITY;
       if (lane == 0) vote[BUF][w] = marg;
     }
   };
