@@ -17,7 +17,7 @@ from paper_2607_25291_amd import binding as B
 from paper_2607_25291_amd.calibrate import delta_for_budget
 from paper_2607_25291_amd.inputs import WORKLOADS, Workload, make_inputs, random_inputs
 from tests import parity as PR
-from tests.gpu_util import Run, bf16_to_f64, dev, host_bits, tau_of
+from tests.gpu_util import Run, bf16_to_f64, dev, host_bits, tau_of, torch
 
 pytestmark = pytest.mark.gpu
 
@@ -161,6 +161,38 @@ def test_osk_skip_parity(case):
     assert np.array_equal(gn, ora["n_computed"])
     mx, mean = PR.check_output(bf16_to_f64(host_bits(o)), ora["o"])
     say(f"  O max-abs {mx:.2e} mean-abs {mean:.2e}")
+
+
+def test_osk_decisions_without_margin_log(case):
+    """Without a margin log the kernel takes each skip decision from whether some row's margin
+    reaches tau, instead of from the tile's maximum margin; decisions, counts and O must be the
+    same bit for bit. Thresholds: the calibrated one, tau = 0 (Delta = L: only blocks where some
+    row's maximum does not fall are computed) and a small Delta (almost nothing is skipped)."""
+    w, run = case["w"], case["run"]
+    say("[osk decisions without margin log]", w.name)
+    order, count = _oracle_lists(case)
+    od, cd = dev(order), dev(count)
+    _, _, margin, _ = run.osk(od, cd, None)
+    gm = margin.cpu().numpy()
+    total = w.batch * w.n_q_heads * O.causal_blocks(w.seq_len, w.block)
+    G = w.n_q_heads // w.n_kv_heads
+    mask = np.arange(w.n_blocks)[None, None, None, :] < np.repeat(count, G, axis=1)[..., None]
+    delta_cal, _, _ = delta_for_budget(gm[mask], int(count.sum()) * G, total, w.osk_budget,
+                                       w.seq_len)
+    t = torch()
+    for delta in (delta_cal, float(w.seq_len), w.seq_len * math.exp(-8.0)):
+        sk = B.skip(B.SKIP_ROWMAX, delta)
+        o_ref, vis_ref, _, nco_ref = run.osk(od, cd, sk)
+        o = t.zeros_like(o_ref)
+        vis = t.zeros_like(vis_ref)
+        nco = t.full_like(nco_ref, -1)
+        B.cosa_osk_attention(run.problem, run.q, run.k, run.v, od, cd, sk, o, vis, None, nco)
+        t.cuda.synchronize()
+        assert np.array_equal(vis.cpu().numpy(), vis_ref.cpu().numpy()), delta
+        assert np.array_equal(nco.cpu().numpy(), nco_ref.cpu().numpy()), delta
+        assert np.array_equal(host_bits(o), host_bits(o_ref)), delta
+        skipped = int((vis.cpu().numpy() == B.VISIT_SKIPPED).sum())
+        say(f"  delta {delta:.4g}: {skipped} skipped of {int(count.sum()) * G} listed")
 
 
 def test_prefill_matches_stages(case):
