@@ -1,0 +1,60 @@
+"""Stage-1 selection on long rows: nb = 4096 candidate blocks per row (a 512K-token sequence at
+b = 128), the row length where the kernel's LDS exceeds the default dynamic limit and the kept set
+outgrows one wavefront's sort.
+
+The scores and flags are seeded random inputs fed to both sides: the HIP selection must match the
+oracle's rule (Sec. 4.2 "Flag-grouped sorting", Eq. (mkap)) bit for bit on sampled rows, for the
+fraction cut at two budgets (kept sets of up to 82 and up to 410 blocks), the ascending visit
+order, and keep-all.
+"""
+import sys
+
+import numpy as np
+import pytest
+
+from oracle import cosa_oracle as O
+from paper_2607_25291_amd import binding as B
+from tests.gpu_util import torch
+
+pytestmark = pytest.mark.gpu
+
+NB = 4096
+
+
+def say(*a):
+    print(*a, flush=True)
+    sys.stdout.flush()
+
+
+@pytest.fixture(scope="module")
+def rows():
+    rng = np.random.default_rng(20261202)
+    score = rng.gamma(2.0, 1.0, size=(1, 1, NB, NB)).astype(np.float32)
+    hrm = (rng.random((1, 1, NB, NB)) < 0.002).astype(np.uint8)
+    sample = sorted(set([0, 1, 2, 127, 128, 129, 511, 512, 1023, 1024, 2047, 2048, 3071, 4094, 4095]
+                        + [int(x) for x in rng.integers(0, NB, 16)]))
+    return score, hrm, sample
+
+
+@pytest.mark.parametrize("mode,value,order_mode", [
+    (B.SELECT_FRACTION, 0.02, B.ORDER_KAP), (B.SELECT_FRACTION, 0.10, B.ORDER_KAP),
+    (B.SELECT_FRACTION, 0.10, B.ORDER_ASCENDING), (B.SELECT_ALL, 1.0, B.ORDER_KAP)])
+def test_select_long_rows(rows, mode, value, order_mode):
+    score, hrm, sample = rows
+    say(f"[select long rows] nb={NB} mode={mode} value={value} order={order_mode}")
+    t = torch()
+    p = B.Problem(1, 1, 1, NB * 128, 128, 128, 16)
+    sd = t.from_numpy(score).cuda()
+    hd = t.from_numpy(hrm).cuda()
+    order = t.full((1, 1, NB, NB), -7, dtype=t.int32, device="cuda")
+    count = t.full((1, 1, NB), -7, dtype=t.int32, device="cuda")
+    B.cosa_kap_select_ordered(p, sd, hd, B.select(mode, value, order_mode), order, count)
+    t.cuda.synchronize()
+    units = [(0, 0, i) for i in sample]
+    oo, oc = O.kap_select(score.astype(np.float64), hrm, mode=mode, value=value,
+                          order_mode=order_mode, units=units)
+    go, gc = order.cpu().numpy(), count.cpu().numpy()
+    for (n, g, i) in units:
+        assert gc[n, g, i] == oc[n, g, i], i
+        assert np.array_equal(go[n, g, i], oo[n, g, i]), i
+    say(f"  {len(units)} rows identical; largest kept set {int(gc.max())}")
