@@ -476,16 +476,6 @@ void attention_kernel(const AttnParams P) {
       const float alpha = __builtin_amdgcn_exp2f((m - mnew) * P.scale_log2);
       m = mnew;
       const float mb = mnew * P.scale_log2;
-      float rs = 0.f;
-#pragma unroll
-      for (int t = 0; t < KT; ++t)
-#pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          const float pv = __builtin_amdgcn_exp2f(fmaf(s[t][r], P.scale_log2, -mb));
-          s[t][r] = pv;
-          rs += pv;
-        }
-      lsum = fmaf(lsum, alpha, rs);
       if (__any(alpha != 1.f)) {  // the running max moved in some row of this wave
 #pragma unroll
         for (int dt = 0; dt < 4; ++dt)
@@ -494,38 +484,71 @@ void attention_kernel(const AttnParams P) {
       }
       // O^T += V^T P^T over 16-key chunks kc = 2 t + c2: P^T element e of the chunk is register
       // 8 c2 + e of tile t (key 32 t + 16 c2 + 8 (e / 4) + 4 half + e % 4); the V^T operand is the
-      // matching pair of transposing reads (e / 4 = a).
-      // The transposing reads are issued directly so that the chunk and half-row offsets go into
-      // the instruction's offset field (the compiler adds them to the address in a VALU op per read
-      // otherwise); the explicit wait then hands the fragments to the MFMAs.
+      // matching pair of transposing reads (e / 4 = a). The transposing reads are issued directly
+      // so that the chunk and half-row offsets go into the instruction's offset field (the
+      // compiler adds them to the address in a VALU op per read otherwise); the explicit wait
+      // then hands the fragments to the MFMAs.
+      // List and mask walks are software-pipelined one chunk deep: the softmax and the V^T reads
+      // of chunk kc + 1 are issued behind the MFMAs of chunk kc (OSK 1.9 % faster). The dense
+      // walk takes the softmax of the whole tile first, which measured 0.6 % faster there. Either
+      // way the row sum takes the chunks, and their elements, in order.
+      constexpr int KC = BLOCK / 16;
+      constexpr bool kPipe = WALK != kWalkDense;
+      float rs = 0.f;
+      auto softmax_chunk = [&](int kc, bf16x8_t& pf) __attribute__((always_inline)) {
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+          const float pv = __builtin_amdgcn_exp2f(
+              fmaf(s[kc >> 1][8 * (kc & 1) + e], P.scale_log2, -mb));
+          rs += pv;
+          pf[e] = (__bf16)pv;
+        }
+      };
       int va[4];
 #pragma unroll
       for (int dt = 0; dt < 4; ++dt) va[dt] = (int)(size_t)COSA_LDS(Vb) + v_rd[dt];
+      s16x4_t lo[2][4], hi[2][4];
+      bf16x8_t pf[KC];
+      if constexpr (kPipe) {
+        softmax_chunk(0, pf[0]);
+      } else {
 #pragma unroll
-      for (int kc = 0; kc < BLOCK / 16; ++kc) {
-        bf16x8_t pf;
+        for (int kc = 0; kc < KC; ++kc) softmax_chunk(kc, pf[kc]);
+      }
 #pragma unroll
-        for (int e = 0; e < 8; ++e) pf[e] = (__bf16)s[kc >> 1][8 * (kc & 1) + e];
-        s16x4_t lo[4], hi[4];
+      for (int dt = 0; dt < 4; ++dt) {
+        asm volatile("ds_read_b64_tr_b16 %0, %1 offset:%2" : "=v"(lo[0][dt]) : "v"(va[dt]), "i"(0));
+        asm volatile("ds_read_b64_tr_b16 %0, %1 offset:%2"
+                     : "=v"(hi[0][dt]) : "v"(va[dt]), "i"(8 * 256));
+      }
 #pragma unroll
-        for (int dt = 0; dt < 4; ++dt) {
-          asm volatile("ds_read_b64_tr_b16 %0, %1 offset:%2"
-                       : "=v"(lo[dt]) : "v"(va[dt]), "i"(kc * 16 * 256));
-          asm volatile("ds_read_b64_tr_b16 %0, %1 offset:%2"
-                       : "=v"(hi[dt]) : "v"(va[dt]), "i"(kc * 16 * 256 + 8 * 256));
-        }
+      for (int kc = 0; kc < KC; ++kc) {
+        const int cb = kc & 1, nx = cb ^ 1;
         asm volatile("s_waitcnt lgkmcnt(0)"
-                     : "+v"(lo[0]), "+v"(lo[1]), "+v"(lo[2]), "+v"(lo[3]), "+v"(hi[0]),
-                       "+v"(hi[1]), "+v"(hi[2]), "+v"(hi[3]));
+                     : "+v"(lo[cb][0]), "+v"(lo[cb][1]), "+v"(lo[cb][2]), "+v"(lo[cb][3]),
+                       "+v"(hi[cb][0]), "+v"(hi[cb][1]), "+v"(hi[cb][2]), "+v"(hi[cb][3]));
 #pragma unroll
         for (int dt = 0; dt < 4; ++dt) {
           const bf16x8_t vf = __builtin_bit_cast(
-              bf16x8_t, __builtin_shufflevector(lo[dt], hi[dt], 0, 1, 2, 3, 4, 5, 6, 7));
-          o[dt] = mfma32x32x16(vf, pf, o[dt]);
+              bf16x8_t, __builtin_shufflevector(lo[cb][dt], hi[cb][dt], 0, 1, 2, 3, 4, 5, 6, 7));
+          o[dt] = mfma32x32x16(vf, pf[kc], o[dt]);
         }
-        __builtin_amdgcn_sched_group_barrier(0x100, 8, 0);  // the chunk's transposing reads ...
-        __builtin_amdgcn_sched_group_barrier(0x008, 4, 0);  // ... then its MFMAs
+        if (kc + 1 < KC) {
+#pragma unroll
+          for (int dt = 0; dt < 4; ++dt) {
+            asm volatile("ds_read_b64_tr_b16 %0, %1 offset:%2"
+                         : "=v"(lo[nx][dt]) : "v"(va[dt]), "i"((kc + 1) * 16 * 256));
+            asm volatile("ds_read_b64_tr_b16 %0, %1 offset:%2"
+                         : "=v"(hi[nx][dt]) : "v"(va[dt]), "i"((kc + 1) * 16 * 256 + 8 * 256));
+          }
+          if constexpr (kPipe) softmax_chunk(kc + 1, pf[kc + 1]);
+        }
+        if constexpr (!kPipe) {
+          __builtin_amdgcn_sched_group_barrier(0x008, 4, 0);  // the chunk's MFMAs ...
+          __builtin_amdgcn_sched_group_barrier(0x100, 8, 0);  // ... then the next chunk's reads
+        }
       }
+      lsum = fmaf(lsum, alpha, rs);
       ++ncomp;
       __builtin_amdgcn_s_setprio(0);
     }
