@@ -487,7 +487,8 @@ void attention_kernel(const AttnParams P) {
       // matching pair of transposing reads (e / 4 = a). The transposing reads are issued directly
       // so that the chunk and half-row offsets go into the instruction's offset field (the
       // compiler adds them to the address in a VALU op per read otherwise); the explicit wait
-      // then hands the fragments to the MFMAs.
+      // names the fragments, which hands them to the MFMAs and keeps their registers reserved
+      // until the data has landed (the compiler does not see the reads as loads).
       // List and mask walks are software-pipelined: the V^T reads of chunk kc + 1 and the softmax
       // of chunk kc + 2 are issued behind the MFMAs of chunk kc (OSK 2.5 % faster). The dense
       // walk takes the softmax of the whole tile first, which measured 0.6 % faster there. Either
