@@ -543,8 +543,8 @@ def main():
                     help="run one plain device copy of this many MiB first (counter calibration)")
     args = ap.parse_args()
     if args.gpus != 1:
-        print(f"bench.py: this build runs on one GPU only (asked for --gpus {args.gpus}); the "
-              "multi-GPU sharding of this path is a design note, not an implemented mode.",
+        print(f"bench.py: runs on one GPU only (asked for --gpus {args.gpus}); the path is not "
+              "sharded across GPUs.",
               file=sys.stderr)
         sys.exit(2)
     if args.sweep:
