@@ -107,12 +107,12 @@ __device__ __forceinline__ void copy_page(__amdgpu_buffer_rsrc_t rs, char* dst, 
 }
 
 // Paged variant (Sec. 4.3 "Physical jumping over pages"): the block's rows live in physical pages of
-// 2^log2p >= 16 tokens of a [n_pages, Hkv, page, d] cache, so a 4-row chunk never straddles two
-// pages. Here wave w moves the consecutive chunks w * CPW .. w * CPW + CPW - 1, so it looks up a
-// physical page and builds a buffer resource only where its rows enter a new page (once or twice
-// per block); the chunks inside a page are immediate offsets from it. Lane k of `tbl` holds the
-// physical page of the block's k-th page-sized segment (segment 0 when a page holds the block).
-// Addressing stays 64-bit for caches of any size.
+// 2^log2p >= 16 tokens of a [n_pages, Hkv, page, d] cache. Wave w moves the consecutive chunks
+// w * CPW .. w * CPW + CPW - 1 in runs of four (16 rows): a run starts 16-aligned, so it lies inside
+// one physical page whatever the page size, and each run takes one page lookup and one buffer
+// resource, its chunks immediate offsets from it (no per-chunk test for a page boundary). Lane k of
+// `tbl` holds the physical page of the block's k-th page-sized segment (segment 0 when a page holds
+// the block). Addressing stays 64-bit for caches of any size.
 template <int BLOCK, int NW, bool IS_K>
 __device__ __forceinline__ void copy_page_paged(const uint16_t* cache, long long page_elems,
                                                 int tbl, int first_row, int log2p, char* dst,
@@ -124,26 +124,24 @@ __device__ __forceinline__ void copy_page_paged(const uint16_t* cache, long long
   // Opaque wave index: the per-chunk offsets are formed here instead of being hoisted out of the
   // page loop into scalar registers.
   asm volatile("" : "+s"(w));
-  __amdgpu_buffer_rsrc_t rs;
-  int u0 = 0;
 #pragma unroll
-  for (int u = 0; u < CPW; ++u) {
-    const int row_in_block = (w * CPW + u) * 4;
-    const int in_page = (first_row + row_in_block) & page_mask;
-    if (u == 0 || in_page == 0) {  // the wave's rows enter a (new) physical page
-      const long long phys = __builtin_amdgcn_readlane(tbl, row_in_block >> log2p);
-      const uint16_t* base = cache + phys * page_elems + (long long)in_page * kHeadDim;
-      rs = __builtin_amdgcn_make_buffer_rsrc((void*)base, (short)0,
-                                             ((page_mask + 1) - in_page) * kHeadDim * 2,
-                                             0x00020000);
-      u0 = u;
+  for (int run = 0; run < CPW / 4; ++run) {
+    const int row0 = (w * CPW + 4 * run) * 4;  // first row of the run within the block
+    const int in_page = (first_row + row0) & page_mask;
+    const long long phys = __builtin_amdgcn_readlane(tbl, row0 >> log2p);
+    const uint16_t* base = cache + phys * page_elems + (long long)in_page * kHeadDim;
+    const __amdgpu_buffer_rsrc_t rs =
+        __builtin_amdgcn_make_buffer_rsrc((void*)base, (short)0, 16 * kHeadDim * 2, 0x00020000);
+#pragma unroll
+    for (int u4 = 0; u4 < 4; ++u4) {
+      const int u = 4 * run + u4;
+      const int row = 4 * (w * CPW + u) + (lane >> 4);
+      const int stored = lane & 15;
+      const int slot = IS_K ? (stored ^ (row & 15)) : (stored ^ ((row & 3) << 2));
+      const int voff = (lane >> 4) * (kHeadDim * 2) + slot * 16;
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, COSA_LDS(dst + (w * CPW + u) * 1024), 16, voff,
+                                               u4 * 1024, 0, 0);
     }
-    const int row = 4 * (w * CPW + u) + (lane >> 4);
-    const int stored = lane & 15;
-    const int slot = IS_K ? (stored ^ (row & 15)) : (stored ^ ((row & 3) << 2));
-    const int voff = (lane >> 4) * (kHeadDim * 2) + slot * 16;
-    __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, COSA_LDS(dst + (w * CPW + u) * 1024), 16, voff,
-                                             (u - u0) * 1024, 0, 0);
   }
 }
 
