@@ -135,11 +135,21 @@ def cpu_baseline(w, q, k, v, gpu_count, gpu_ncomp, delta, budget_s: float = 15.0
                        for (n, h, i) in q_units)
         n_kv += len(kv_units)
         n_q += len(q_units)
+    # the oracle's dense tiles, for the per-block rate only (a few query blocks of one head)
+    dense_blocks = sorted(rng.choice(nb, size=min(4, nb), replace=False).tolist())
+    t0 = time.perf_counter()
+    O.dense_attention(q, k, v, block=w.block, units=[(0, 0, i) for i in dense_blocks])
+    t_dense = time.perf_counter() - t0
+    dense_smp = sum(i + 1 for i in dense_blocks)
     # causal cost model: proxy unit ~ (i+1) keys; OSK tile ~ listed + computed blocks
     kap_all = w.batch * w.n_kv_heads * nb * (nb + 1) / 2
     osk_all = float(np.repeat(gpu_count, G, axis=1).sum() + gpu_ncomp.sum())
     est_s = t_kap * kap_all / kap_smp + t_osk * osk_all / max(osk_smp, 1)
+    dense_all = w.batch * w.n_q_heads * nb * (nb + 1) / 2
     return {"value": est_s * 1e3, "unit": "ms/layer", "cores": int(cores), "kind": "oracle",
+            "seconds_per_block": {"proxy_row": t_kap / kap_smp, "osk_tile": t_osk / max(osk_smp, 1),
+                                  "dense_tile": t_dense / dense_smp},
+            "dense_ms_per_layer": t_dense / dense_smp * dense_all * 1e3,
             "sample": (f"{n_kv} proxy units (2 KV heads x random query blocks) and {n_q} OSK "
                        f"tiles (2 query heads x the same query blocks) of the same inputs, "
                        f"{t_kap + t_osk:.1f} s of oracle time, scaled to one layer by the causal "
