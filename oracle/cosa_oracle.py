@@ -25,8 +25,10 @@ Readings of points where the paper is silent or loose (all indices 0-based):
 * GQA: one ordered list per KV head; the block score sums over the sampled rows of all query heads of
   the group and the HRM flag is an OR over them. The skip vote stays per (query head, query block).
 * K_i under a fractional budget is min(i+1, max(1, ceil(B1 (i+1)))) over the i+1 causal
-  candidates, with B1 taken at 1e-6 resolution and the product formed in integers; top-p keeps the shortest prefix of the HRM-first order whose score mass reaches p of
-  the row total. Equal sort keys are ordered by ascending block index.
+  candidates, with B1 taken at 1e-6 resolution and the product formed in integers; top-p keeps the
+  shortest prefix of the HRM-first order whose score mass reaches p of the row total, both sums in
+  float64 taken term by term (the total over ascending block index, the running mass in list
+  order). Equal sort keys are ordered by ascending block index.
 * HRM is exact equality with the row maximum in the working precision.
 * tau is computed in float64 from the float32 Delta and rounded once to float32.
 * A ragged last block (seq_len not a multiple of b) has fewer rows/keys; nothing else changes.
@@ -203,7 +205,8 @@ def stage1_count(mode: int, value: float, n_cand: int, scores_sorted: Sequence[f
 
     Fraction: K_i = B1 * (candidates) (Eq. (mkap)), rounded up and clamped to [1, n_cand], over the
     causal candidates j <= i. Top-p: the shortest prefix of the HRM-first order whose score mass
-    reaches p of the row total (Algorithm A, proxy stage).
+    reaches p of the row total (Algorithm A, proxy stage). The running mass is a float64 sum taken
+    in list order, one term after another, against p (at 1e-6 resolution) times the total.
     """
     if mode == SELECT_ALL:
         return n_cand
@@ -241,7 +244,10 @@ def kap_select(score, hrm, *, mode: int, value: float, order_mode: int = ORDER_K
         rest = [j for j in cands if not hrm[n, g, i, j]]
         by_score = lambda j: (-float(score[n, g, i, j]), j)
         rho = sorted(hrm_grp, key=by_score) + sorted(rest, key=by_score)
-        total = float(sum(float(score[n, g, i, j]) for j in cands))
+        # the row mass: a float64 sum taken in ascending block index, one term after another
+        total = 0.0
+        for j in cands:
+            total += float(score[n, g, i, j])
         K = stage1_count(mode, value, i + 1, [float(score[n, g, i, j]) for j in rho], total)
         kept = rho[:K]
         if order_mode == ORDER_ASCENDING:

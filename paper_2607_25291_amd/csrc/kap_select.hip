@@ -9,10 +9,13 @@
 // group first, each group by descending score). By fraction, K_i follows from the row length
 // (integer arithmetic on the budget in millionths): a radix selection over 8-bit digits finds the
 // K_i-th largest key, and only the keys at or above it are sorted (bitonic, in LDS; within one
-// wavefront when at most 128). By top-p the cut depends on the sorted scores (fp64 prefix sums),
-// so the whole row is sorted, as it is when every candidate is kept. Ascending visit order
-// re-sorts the kept set by block index. Keys are distinct, so every path yields the one ordering.
-// The row of `order` is written in full: K_i block ids followed by -1.
+// wavefront when at most 128). By top-p the cut depends on the sorted scores, so the whole row is
+// sorted, as it is when every candidate is kept. The top-p sums run in fp64 in one fixed order, on
+// one lane: the row total over ascending block index, then the running mass down the sorted order
+// until it reaches p of the total (each score widens exactly, so the cut depends on nothing but
+// that order). Ascending visit order re-sorts the kept set by block index. Keys are distinct, so
+// every path yields the one ordering. The row of `order` is written in full: K_i block ids
+// followed by -1. Scores are expected to be finite and non-negative (the proxy's are).
 #include <mutex>
 
 #include "cosa_device.h"
@@ -134,8 +137,6 @@ __device__ void select_top(const uint64_t* keys, int n, int K, int tid, uint32_t
 
 __global__ __launch_bounds__(kSelThreads) void kap_select_kernel(const SelParams P) {
   extern __shared__ uint64_t keys[];
-  __shared__ double part[kSelThreads];
-  __shared__ double total_s;
   __shared__ int kcut;
   __shared__ uint32_t hist[256];
   __shared__ uint64_t sel_prefix;
@@ -189,32 +190,24 @@ __global__ __launch_bounds__(kSelThreads) void kap_select_kernel(const SelParams
     bitonic_desc(keys, n2, tid);
     K = n;
   } else {  // COSA_SELECT_TOP_P: shortest prefix reaching p of the row mass
+    // The row total in ascending block index, read before the sort permutes the keys; the kept
+    // count from the running mass in sorted order. Both are sequential fp64 sums on one lane, so
+    // the cut is the same for any launch shape.
+    double total = 0.0;
+    if (tid == 0)
+      for (int t = 0; t < n; ++t) total += (double)key_score(keys[t]);
+    __syncthreads();
     bitonic_desc(keys, n2, tid);
-    const int seg = (n + kSelThreads - 1) / kSelThreads;
-    const int lo = tid * seg, hi = min(n, lo + seg);
-    double ps = 0.0;
-    for (int k = lo; k < hi; ++k) ps += (double)key_score(keys[k]);
-    part[tid] = ps;
-    __syncthreads();
     if (tid == 0) {
-      double run = 0.0;
-      for (int t = 0; t < kSelThreads; ++t) {
-        const double v = part[t];
-        part[t] = run;
-        run += v;
+      const double target = ((double)P.a.value_micro / 1e6) * total;
+      double cum = 0.0;
+      int k = 0;
+      while (k < n) {
+        cum += (double)key_score(keys[k]);
+        ++k;
+        if (cum >= target) break;
       }
-      total_s = run;
-      kcut = n;
-    }
-    __syncthreads();
-    const double target = ((double)P.a.value_micro / 1e6) * total_s;
-    double cum = part[tid];
-    for (int k = lo; k < hi; ++k) {
-      cum += (double)key_score(keys[k]);
-      if (cum >= target) {
-        atomicMin(&kcut, k + 1);
-        break;
-      }
+      kcut = k;
     }
     __syncthreads();
     K = kcut;

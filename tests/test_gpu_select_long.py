@@ -1,11 +1,13 @@
-"""Stage-1 selection on long rows: nb = 4096 candidate blocks per row (a 512K-token sequence at
-b = 128), the row length where the kernel's LDS exceeds the default dynamic limit and the kept set
-outgrows one wavefront's sort.
+"""Stage-1 selection on long rows: nb = 1024 candidate blocks per row (the 128K benchmark at
+b = 128) and nb = 4096 (a 512K-token sequence), the row lengths where the kernel's LDS exceeds the
+default dynamic limit, the kept set outgrows one wavefront's sort and the top-p running mass covers
+hundreds of entries.
 
 The scores and flags are seeded random inputs fed to both sides: the HIP selection must match the
-oracle's rule (Sec. 4.2 "Flag-grouped sorting", Eq. (mkap)) bit for bit on sampled rows, for the
-fraction cut at two budgets (kept sets of up to 82 and up to 410 blocks), the ascending visit
-order, and keep-all.
+oracle's rule (Sec. 4.2 "Flag-grouped sorting", Eq. (mkap); Algorithm A, proxy stage, top-p) bit for
+bit on sampled rows, for the fraction cut at two budgets (kept sets of up to 82 and up to 410
+blocks), top-p at p = 0.5 and 0.95 (the paper's operating point) in both visit orders, the
+ascending visit order, and keep-all.
 """
 import sys
 
@@ -18,29 +20,32 @@ from tests.gpu_util import torch
 
 pytestmark = pytest.mark.gpu
 
-NB = 4096
-
 
 def say(*a):
     print(*a, flush=True)
     sys.stdout.flush()
 
 
-@pytest.fixture(scope="module")
-def rows():
-    rng = np.random.default_rng(20261202)
-    score = rng.gamma(2.0, 1.0, size=(1, 1, NB, NB)).astype(np.float32)
-    hrm = (rng.random((1, 1, NB, NB)) < 0.002).astype(np.uint8)
-    sample = sorted(set([0, 1, 2, 127, 128, 129, 511, 512, 1023, 1024, 2047, 2048, 3071, 4094, 4095]
-                        + [int(x) for x in rng.integers(0, NB, 16)]))
-    return score, hrm, sample
+@pytest.fixture(scope="module", params=[1024, 4096])
+def rows(request):
+    nb = request.param
+    rng = np.random.default_rng(20261202 + nb)
+    score = rng.gamma(2.0, 1.0, size=(1, 1, nb, nb)).astype(np.float32)
+    hrm = (rng.random((1, 1, nb, nb)) < 0.002).astype(np.uint8)
+    fixed = [0, 1, 2, 127, 128, 129, 255, 256, 257, 511, 512, nb // 2 - 1, nb // 2, nb - 2, nb - 1]
+    if nb > 1024:
+        fixed += [1023, 1024, 2047, 2048, 3071]
+    sample = sorted(set(fixed + [int(x) for x in rng.integers(0, nb, 16)]))
+    return nb, score, hrm, sample
 
 
 @pytest.mark.parametrize("mode,value,order_mode", [
     (B.SELECT_FRACTION, 0.02, B.ORDER_KAP), (B.SELECT_FRACTION, 0.10, B.ORDER_KAP),
-    (B.SELECT_FRACTION, 0.10, B.ORDER_ASCENDING), (B.SELECT_ALL, 1.0, B.ORDER_KAP)])
+    (B.SELECT_FRACTION, 0.10, B.ORDER_ASCENDING), (B.SELECT_ALL, 1.0, B.ORDER_KAP),
+    (B.SELECT_TOP_P, 0.5, B.ORDER_KAP), (B.SELECT_TOP_P, 0.95, B.ORDER_KAP),
+    (B.SELECT_TOP_P, 0.95, B.ORDER_ASCENDING)])
 def test_select_long_rows(rows, mode, value, order_mode):
-    score, hrm, sample = rows
+    NB, score, hrm, sample = rows
     say(f"[select long rows] nb={NB} mode={mode} value={value} order={order_mode}")
     t = torch()
     p = B.Problem(1, 1, 1, NB * 128, 128, 128, 16)
@@ -57,4 +62,6 @@ def test_select_long_rows(rows, mode, value, order_mode):
     for (n, g, i) in units:
         assert gc[n, g, i] == oc[n, g, i], i
         assert np.array_equal(go[n, g, i], oo[n, g, i]), i
-    say(f"  {len(units)} rows identical; largest kept set {int(gc.max())}")
+    kept = [int(gc[0, 0, i]) for i in sample]
+    say(f"  {len(units)} rows identical; largest kept set {max(kept)}, "
+        f"kept {sum(kept)} of {sum(i + 1 for i in sample)} candidates on the sampled rows")

@@ -98,3 +98,40 @@ def test_ascending_mode_same_set():
     for i in range(nb):
         K = c1[0, 0, i]
         assert sorted(o1[0, 0, i, :K].tolist()) == o2[0, 0, i, :K].tolist()
+
+
+@pytest.mark.parametrize("p", [0.3, 0.5, 0.9, 0.95, 0.999])
+def test_top_p_exact_rational(p):
+    """Top-p count against exact rational arithmetic: the smallest k whose prefix mass (in the
+    HRM-first order) reaches p of the row mass. The oracle sums in float64, so the two may differ
+    only where the exact prefix mass lies within float64 rounding of the target; such rows are
+    counted and must be rare, every other row must agree exactly."""
+    from fractions import Fraction
+    nb = 64
+    rng = np.random.default_rng(11)
+    s = rng.gamma(0.7, 1.0, (1, 1, nb, nb)).astype(np.float32).astype(np.float64)
+    h = (rng.uniform(size=(1, 1, nb, nb)) < 0.1).astype(np.uint8)
+    for i in range(nb):
+        s[0, 0, i, i + 1:] = 0
+        h[0, 0, i, i + 1:] = 0
+    order, count = O.kap_select(s, h, mode=O.SELECT_TOP_P, value=np.float32(p))
+    pm = Fraction(O.budget_micro(np.float32(p)), 10 ** 6)
+    near = 0
+    for i in range(nb):
+        row = [(-int(h[0, 0, i, j]), -s[0, 0, i, j], j) for j in range(i + 1)]
+        rho = [j for (_, _, j) in sorted(row)]
+        total = sum(Fraction(float(s[0, 0, i, j])) for j in range(i + 1))
+        target = pm * total
+        cum, k_exact, masses = Fraction(0), i + 1, []
+        for k, j in enumerate(rho):
+            cum += Fraction(float(s[0, 0, i, j]))
+            masses.append(cum)
+            if cum >= target:
+                k_exact = k + 1
+                break
+        K = int(count[0, 0, i])
+        assert order[0, 0, i, :K].tolist() == rho[:K]
+        if K != k_exact:
+            near += 1
+            assert abs(float(masses[min(K, k_exact) - 1] - target)) <= 1e-12 * float(total), i
+    assert near <= 1
