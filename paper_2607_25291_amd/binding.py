@@ -102,6 +102,12 @@ def lib():
         if not os.path.exists(LIB_PATH):
             raise RuntimeError(f"{LIB_PATH} is missing: build it with "
                                "`python -m paper_2607_25291_amd.build_lib`")
+        # The library's HIP calls must bind to the HIP runtime that PyTorch loaded, so that the
+        # tensors, streams and events it hands over belong to the same runtime. Importing torch
+        # first puts that runtime in the process's global symbol scope, where the dynamic linker
+        # resolves the library's HIP symbols; loaded the other way round, the library would start
+        # a second HIP runtime of its own, which does not share torch's streams or device state.
+        import torch  # noqa: F401
         L = ctypes.CDLL(LIB_PATH)
         P, S, vp = ctypes.POINTER(CosaProblem), ctypes.c_int, ctypes.c_void_p
         L.cosa_status_string.restype = ctypes.c_char_p
