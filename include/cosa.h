@@ -284,6 +284,30 @@ cosa_status cosa_prefill(const cosa_problem* problem, const void* q, const void*
                          const cosa_select* select, const cosa_skip* skip, void* workspace,
                          size_t workspace_bytes, void* o, void* stream);
 
+/* Largest workspace cosa_prefill_noalloc can use: 96 MiB, which holds the workspace of one
+ * 128K-token layer with 8 KV heads (88 MiB). */
+#define COSA_NOALLOC_SCRATCH_BYTES (96u * 1024u * 1024u)
+
+/*
+ * For callers that cannot allocate device memory (code under HIP graph capture, tight serving
+ * loops, harnesses that forbid allocation): cosa_prefill with its workspace in a static scratch
+ * array of the library instead of a caller buffer. Same arguments, results and errors as
+ * cosa_prefill otherwise; the caller still owns q, k, v and o.
+ *   - Returns COSA_ERR_WORKSPACE and enqueues nothing when cosa_prefill_workspace_bytes(problem)
+ *     exceeds COSA_NOALLOC_SCRATCH_BYTES.
+ *   - Allocates nothing: no hipMalloc, hipFree or allocating library routine. The scratch array
+ *     exists once per GPU the library runs on and is held until the process ends; its device
+ *     address is looked up on the first call on each GPU (the GPU of `stream`, the current device
+ *     for the null stream).
+ *   - Every call on one GPU uses that GPU's single array, which keeps the last call's contents
+ *     (they are not exposed). Calls that overlap on one GPU (several streams, or several host
+ *     threads) race on it: the caller must serialise them. Whatever must start at zero is cleared
+ *     by a kernel on `stream` (no memset node).
+ */
+cosa_status cosa_prefill_noalloc(const cosa_problem* problem, const void* q, const void* k,
+                                 const void* v, const cosa_select* select, const cosa_skip* skip,
+                                 void* o, void* stream);
+
 /*
  * cosa_kap_score with K read from a paged cache (kv->v_cache is not used and may be NULL):
  * sampled key c (token c * stride) of KV head g is row (token % page_size) of physical page

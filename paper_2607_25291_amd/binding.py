@@ -135,6 +135,9 @@ def lib():
         L.cosa_prefill.restype = S
         L.cosa_prefill.argtypes = [P, vp, vp, vp, ctypes.POINTER(CosaSelect),
                                    ctypes.POINTER(CosaSkip), vp, ctypes.c_size_t, vp, vp]
+        L.cosa_prefill_noalloc.restype = S
+        L.cosa_prefill_noalloc.argtypes = [P, vp, vp, vp, ctypes.POINTER(CosaSelect),
+                                           ctypes.POINTER(CosaSkip), vp, vp]
         L.cosa_block_mass.restype = S
         L.cosa_block_mass.argtypes = [P, vp, vp, vp, vp]
         L.cosa_masked_attention.restype = S
@@ -306,6 +309,17 @@ def cosa_prefill(problem, q, k, v, sel: CosaSelect, sk: Optional[CosaSkip], work
     skp = ctypes.byref(sk) if sk is not None else None
     _check(lib().cosa_prefill(ctypes.byref(p), _ptr(q), _ptr(k), _ptr(v), ctypes.byref(sel), skp,
                               _ptr(workspace), workspace_bytes, _ptr(o), _stream(stream)))
+
+
+NOALLOC_SCRATCH_BYTES = 96 * 1024 * 1024
+
+
+def cosa_prefill_noalloc(problem, q, k, v, sel: CosaSelect, sk: Optional[CosaSkip], o,
+                         stream=None):
+    p = _prob(problem)
+    skp = ctypes.byref(sk) if sk is not None else None
+    _check(lib().cosa_prefill_noalloc(ctypes.byref(p), _ptr(q), _ptr(k), _ptr(v),
+                                      ctypes.byref(sel), skp, _ptr(o), _stream(stream)))
 
 
 def _kvref(kv):

@@ -4,12 +4,18 @@
 #include <stdarg.h>
 #include <stdio.h>
 
+#include <mutex>
 #include <string>
 
 #include "cosa.h"
 #include "cosa_internal.h"
 
 static_assert(COSA_MAX_PACKED_SEQS == cosa::kMaxPackedSeqs, "packing limit of the ABI and kernels");
+
+// Workspace of cosa_prefill_noalloc: one copy per GPU, held until the process ends. In host code
+// this name is only a handle for hipGetSymbolAddress; the device address of each GPU's copy is
+// looked up once per device (scratch_of_device) and used everywhere the host needs the array.
+static __device__ __align__(256) unsigned char scratch[COSA_NOALLOC_SCRATCH_BYTES];
 
 namespace {
 
@@ -198,6 +204,42 @@ cosa_workspace_layout layout_of(const cosa::Shape& sh) {
 }
 
 hipStream_t as_stream(void* s) { return reinterpret_cast<hipStream_t>(s); }
+
+// Device address of `scratch` on the GPU that runs `stream` (the current device for the null
+// stream), taken once per device with that device current and kept for later calls.
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_addr[kMaxDevices] = {};
+
+cosa_status scratch_of_device(hipStream_t stream, void** addr) {
+  int cur = 0;
+  hipError_t e = hipGetDevice(&cur);
+  if (e != hipSuccess) return hip_fail(e, "hipGetDevice");
+  int dev = cur;
+  if (stream != nullptr) {
+    hipDevice_t sd;
+    if ((e = hipStreamGetDevice(stream, &sd)) != hipSuccess) return hip_fail(e, "hipStreamGetDevice");
+    dev = (int)sd;
+  }
+  if (dev < 0 || dev >= kMaxDevices)
+    return fail(COSA_ERR_UNSUPPORTED, "device %d (supported: 0 .. %d)", dev, kMaxDevices - 1);
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (g_scratch_addr[dev] == nullptr) {
+    if (dev != cur && (e = hipSetDevice(dev)) != hipSuccess) return hip_fail(e, "hipSetDevice");
+    void* p = nullptr;
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (dev != cur) {
+      const hipError_t e2 = hipSetDevice(cur);
+      if (e == hipSuccess && e2 != hipSuccess) e = e2;
+    }
+    if (e != hipSuccess) return hip_fail(e, "hipGetSymbolAddress(scratch)");
+    if (p == nullptr || reinterpret_cast<uintptr_t>(p) % 256 != 0)
+      return fail(COSA_ERR_HIP, "scratch of device %d at %p is not 256-byte aligned", dev, p);
+    g_scratch_addr[dev] = p;
+  }
+  *addr = g_scratch_addr[dev];
+  return ok();
+}
 
 // Algorithm A end to end; kv == nullptr: contiguous K and V at k, v; vl == nullptr: no packing.
 cosa_status prefill(const cosa_problem* problem, const void* q, const void* k, const void* v,
@@ -493,6 +535,31 @@ cosa_status cosa_prefill(const cosa_problem* problem, const void* q, const void*
                          size_t workspace_bytes, void* o, void* stream) {
   return prefill(problem, q, k, v, nullptr, nullptr, select, skip, workspace, workspace_bytes, o,
                  stream);
+}
+
+cosa_status cosa_prefill_noalloc(const cosa_problem* problem, const void* q, const void* k,
+                                 const void* v, const cosa_select* select, const cosa_skip* skip,
+                                 void* o, void* stream) {
+  cosa::Shape sh;
+  bool empty = false;
+  cosa_status st = make_shape(problem, sh, empty);
+  if (st != COSA_OK) return st;
+  int64_t micro = 0;
+  if ((st = check_select(select, micro)) != COSA_OK) return st;
+  int on = 0;
+  float tau = 0.f;
+  if ((st = check_skip(skip, sh, on, tau)) != COSA_OK) return st;
+  if (empty) return ok();
+  const size_t need = layout_of(sh).total;
+  if (need > (size_t)COSA_NOALLOC_SCRATCH_BYTES)
+    return fail(COSA_ERR_WORKSPACE,
+                "the problem needs %zu bytes of workspace; the static scratch holds %zu "
+                "(use cosa_prefill with a caller workspace)",
+                need, (size_t)COSA_NOALLOC_SCRATCH_BYTES);
+  void* ws = nullptr;
+  if ((st = scratch_of_device(as_stream(stream), &ws)) != COSA_OK) return st;
+  return prefill(problem, q, k, v, nullptr, nullptr, select, skip, ws,
+                 (size_t)COSA_NOALLOC_SCRATCH_BYTES, o, stream);
 }
 
 cosa_status cosa_prefill_paged(const cosa_problem* problem, const void* q, const cosa_paged_kv* kv,

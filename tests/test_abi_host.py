@@ -18,7 +18,8 @@ EXPECTED = {"cosa_status_string", "cosa_last_error", "cosa_kap_score", "cosa_kap
             "cosa_block_mass", "cosa_kap_score_varlen", "cosa_kap_select_ordered_varlen",
             "cosa_osk_attention_varlen", "cosa_dense_attention_varlen", "cosa_prefill_varlen",
             "cosa_prefill_paged_varlen", "cosa_kap_score_workspace_bytes",
-            "cosa_kap_score_staged", "cosa_osk_attention_queue_bytes", "cosa_osk_attention_queued"}
+            "cosa_kap_score_staged", "cosa_osk_attention_queue_bytes", "cosa_osk_attention_queued",
+            "cosa_prefill_noalloc"}
 
 
 def test_header_declares_the_abi():
@@ -301,3 +302,29 @@ def test_delta_for_budget_packed_host_helper():
     d1, k1, _ = delta_for_budget_packed(one, np.full(600, 4096), 2000, 0.2)
     d0, k0, _ = delta_for_budget(one, 600, 2000, 0.2, 4096)
     assert k1 == k0 and abs(d1 - d0) < 1e-9 * d0
+
+
+def test_noalloc_prefill_rejects_before_the_device():
+    """cosa_prefill_noalloc validates like cosa_prefill and refuses a problem whose workspace
+    exceeds its static scratch array, before any HIP call (so this runs without a GPU)."""
+    big = B.Problem(1, 32, 16, 131072, 128, 128, 16)
+    assert B.cosa_prefill_workspace_bytes(big) > B.NOALLOC_SCRATCH_BYTES
+    with pytest.raises(B.CosaError) as e:
+        B.cosa_prefill_noalloc(big, 16, 16, 16, B.select(B.SELECT_FRACTION, 0.1), None, 16,
+                               stream=0)
+    assert e.value.status == B.COSA_ERR_WORKSPACE and "static scratch" in str(e.value)
+    # the 128K benchmark layer (32 / 8 heads) fits
+    assert B.cosa_prefill_workspace_bytes(B.Problem(1, 32, 8, 131072)) <= B.NOALLOC_SCRATCH_BYTES
+    for sel, sk, status in [(B.select(B.SELECT_FRACTION, 0.0), None, B.COSA_ERR_INVALID_ARG),
+                            (B.select(B.SELECT_TOP_P, 1.5), None, B.COSA_ERR_INVALID_ARG),
+                            (B.select(), B.skip(B.SKIP_ROWMAX, 1e9), B.COSA_ERR_INVALID_ARG)]:
+        with pytest.raises(B.CosaError) as e:
+            B.cosa_prefill_noalloc(GOOD, 16, 16, 16, sel, sk, 16, stream=0)
+        assert e.value.status == status
+    # an empty problem is a no-op
+    B.cosa_prefill_noalloc(B.Problem(0, 8, 2, 1024), None, None, None, B.select(), None, None,
+                           stream=0)
+    with pytest.raises(B.CosaError) as e:
+        B.cosa_prefill_noalloc(B.Problem(1, 8, 2, 1024, head_dim=64), 16, 16, 16, B.select(),
+                               None, 16, stream=0)
+    assert e.value.status == B.COSA_ERR_UNSUPPORTED
