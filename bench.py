@@ -99,7 +99,30 @@ def gemm_ceiling(n: int = 16384, reps: int = 5) -> float:
     return 2.0 * n ** 3 / (ms * 1e-3) / 1e12
 
 
-def cpu_baseline(w, q, k, v, gpu_count, gpu_ncomp, delta, budget_s: float = 15.0):
+def copy_bandwidth(mib: int = 1024, reps: int = 10) -> float:
+    """GB/s (bytes read + bytes written) of a plain device-to-device copy of `mib` MiB, the HBM
+    rate a streaming kernel reaches on this GPU, measured in the same run (median of reps)."""
+    import torch
+    n = mib * 2 ** 20 // 4
+    src = torch.ones(n, dtype=torch.float32, device="cuda")
+    dst = torch.empty_like(src)
+    dst.copy_(src)
+    torch.cuda.synchronize()
+    ts = []
+    for _ in range(reps):
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        dst.copy_(src)
+        e1.record()
+        torch.cuda.synchronize()
+        ts.append(e0.elapsed_time(e1))
+    del src, dst
+    torch.cuda.empty_cache()
+    return 2.0 * mib * 2 ** 20 / (float(np.median(ts)) * 1e-3) / 1e9
+
+
+def cpu_baseline(w, q, k, v, gpu_count, gpu_ncomp, delta, budget_s: float = 15.0,
+                 select_mode: int = 0, select_value: float = None):
     """Time the oracle (as it stands) on sampled units of the same workload, scaled to ms/layer.
 
     Units are drawn in rounds (query blocks spread over the causal range, two KV heads / two query
@@ -123,7 +146,8 @@ def cpu_baseline(w, q, k, v, gpu_count, gpu_ncomp, delta, budget_s: float = 15.0
         t0 = time.perf_counter()
         sc, hr = O.kap_score(q, k, n_kv_heads=w.n_kv_heads, block=w.block, stride=w.stride,
                              units=kv_units)
-        order, count = O.kap_select(sc, hr, mode=O.SELECT_FRACTION, value=w.kap_budget,
+        order, count = O.kap_select(sc, hr, mode=select_mode,
+                                    value=w.kap_budget if select_value is None else select_value,
                                     units=kv_units)
         t_kap += time.perf_counter() - t0
         t0 = time.perf_counter()
@@ -551,6 +575,13 @@ def main():
                     help="run the budget / visiting-order sweep instead of the one-line benchmark")
     ap.add_argument("--copy-probe-mib", type=int, default=0,
                     help="run one plain device copy of this many MiB first (counter calibration)")
+    ap.add_argument("--select", choices=["fraction", "top_p"], default="fraction",
+                    help="stage-1 selection: the workload's fractional budget B1 (default), or "
+                         "top-p with mass --p (the paper's own mode; B1 is then an outcome)")
+    ap.add_argument("--p", type=float, default=0.95, help="top-p mass for --select top_p")
+    ap.add_argument("--osk-budget", type=float, default=None,
+                    help="overall budget B2 that Delta is calibrated to (default: the "
+                         "workload's; with --select top_p: half of the realized B1)")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py: runs on one GPU only (asked for --gpus {args.gpus}); the path is not "
@@ -600,7 +631,10 @@ def main():
     keys = ws[lay.keys:lay.keys + stage_bytes]
     queue_bytes = B.cosa_osk_attention_queue_bytes()
     queue = ws[lay.queue:lay.queue + queue_bytes]
-    sel = B.select(B.SELECT_FRACTION, w.kap_budget)
+    if args.select == "top_p":
+        sel = B.select(B.SELECT_TOP_P, args.p)
+    else:
+        sel = B.select(B.SELECT_FRACTION, w.kap_budget)
     kv = None
     if args.page_size:
         # the same K/V placed in a paged cache [n_pages, Hkv, page, d] through a random table
@@ -642,14 +676,23 @@ def main():
     pos = np.arange(nb)[None, None, None, :] < cnt_q[..., None]
     total = w.batch * w.n_q_heads * nb * (nb + 1) // 2
     listed = int(cnt_q.sum())
+    if args.osk_budget is not None:
+        b2_target = args.osk_budget
+    elif args.select == "top_p":
+        b2_target = 0.5 * listed / total
+    else:
+        b2_target = w.osk_budget
     delta, n_skip, b_real = delta_for_budget(margin.cpu().numpy()[pos], listed, total,
-                                             w.osk_budget, w.seq_len)
+                                             b2_target, w.seq_len)
     del margin
     sk = B.skip(B.SKIP_ROWMAX, delta)
     ncomp = torch.zeros((w.batch, w.n_q_heads, nb), dtype=torch.int32, device=dev)
     B.cosa_osk_attention(p, q, k, v, order, count, sk, o, None, None, ncomp)
     ncomp_np = ncomp.cpu().numpy()
-    assert int(ncomp_np.sum()) == listed - n_skip, "calibrated skip count not reproduced"
+    # the kernel computes exactly the visits whose fp32 margin reaches the fp32 threshold; the
+    # calibration's count can differ only where margins closer than fp32 rounding straddle the cut
+    assert abs(int(ncomp_np.sum()) - (listed - n_skip)) <= 2, "calibrated skip count not reproduced"
+    b_real = float(ncomp_np.sum()) / total
     b1_real = listed / total
     log(f"[bench] B1 realized {b1_real:.4f}, B realized {b_real:.4f}, delta {delta:.3f}")
 
@@ -657,16 +700,21 @@ def main():
     for _ in range(args.warmup):
         prefill_step()
     torch.cuda.synchronize()
-    ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    # one event before every step and one after the last, all on the launch stream: the per-step
+    # durations give the median (the headline), their sum the mean
+    evs_step = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps + 1)]
     t_wall = time.perf_counter()
-    ev0.record(stream)
-    for _ in range(args.steps):
+    for kstep in range(args.steps):
+        evs_step[kstep].record(stream)
         prefill_step()
-    ev1.record(stream)
+    evs_step[-1].record(stream)
     torch.cuda.synchronize()
     wall = time.perf_counter() - t_wall
-    ms_step = ev0.elapsed_time(ev1) / args.steps
-    log(f"[bench] cosa_prefill {ms_step:.3f} ms/layer (wall {1e3 * wall / args.steps:.3f})")
+    per_step = [evs_step[a].elapsed_time(evs_step[a + 1]) for a in range(args.steps)]
+    ms_step = float(np.median(per_step))
+    ms_mean = evs_step[0].elapsed_time(evs_step[-1]) / args.steps
+    log(f"[bench] cosa_prefill median {ms_step:.3f} ms/layer, mean {ms_mean:.3f} "
+        f"(wall {1e3 * wall / args.steps:.3f})")
 
     # ---- cold reps: the 256 MB last-level cache (MALL) flushed before each step ----
     # A 512 MiB fill between steps evicts whatever the previous step left there; only the step
@@ -703,7 +751,7 @@ def main():
         e[3].record(stream)
     torch.cuda.synchronize()
     st = np.array([[e[a].elapsed_time(e[a + 1]) for a in range(3)] for e in evs])
-    t_score, t_select, t_osk = np.mean(st, axis=0)
+    t_score, t_select, t_osk = np.median(st, axis=0)
     log(f"[bench] kap_score {t_score:.3f} ms, kap_select {t_select:.3f} ms, osk {t_osk:.3f} ms")
 
     # ---- dense baseline on identical inputs ----
@@ -732,8 +780,12 @@ def main():
     dense_tflops = f_dense / (t_dense * 1e-3) / 1e12 if t_dense else None
     kf, kb = kap_score_work(w.batch, w.n_q_heads, w.n_kv_heads, nb, w.block, w.stride,
                             w.head_dim)
-    traffic = (None if args.page_size
+    traffic = (None if args.page_size or args.select != "fraction"
                else traffic_from_profile("osk_attention", "attention.hip", w.name))
+    kap_traffic = (None if args.page_size
+                   else traffic_from_profile("kap_score", "kap_score.hip", w.name))
+    copy_gbs = copy_bandwidth()
+    log(f"[bench] plain device copy: {copy_gbs:.0f} GB/s (read + write)")
 
     ceiling = None
     if not args.no_gemm_ceiling:
@@ -746,7 +798,11 @@ def main():
     cpu = None
     if not args.no_cpu_baseline:
         log("[bench] timing the oracle on a sample (cpu_baseline)")
-        cpu = cpu_baseline(w, q_np, k_np, v_np, cnt, ncomp_np, delta)
+        if args.select == "top_p":
+            cpu = cpu_baseline(w, q_np, k_np, v_np, cnt, ncomp_np, delta,
+                               select_mode=B.SELECT_TOP_P, select_value=args.p)
+        else:
+            cpu = cpu_baseline(w, q_np, k_np, v_np, cnt, ncomp_np, delta)
 
     out = {
         "metric": "KAP+OSK prefill attention ms/layer at 128K; speedup vs own dense kernel",
@@ -756,6 +812,7 @@ def main():
         "steps": args.steps,
         "warmup": args.warmup,
         "ms_per_step": round(ms_step, 4),
+        "ms_per_step_mean": round(ms_mean, 4),
         "ms_per_step_cold": round(ms_cold, 4),
         "higher_is_better": False,
         "scaling": "weak",
@@ -765,7 +822,9 @@ def main():
         "config": {"workload": w.name, "batch": w.batch, "n_q_heads": w.n_q_heads,
                    "n_kv_heads": w.n_kv_heads, "seq_len": w.seq_len, "head_dim": w.head_dim,
                    "block": w.block, "stride": w.stride, "kap_budget": w.kap_budget,
-                   "osk_budget": w.osk_budget, "select": "fraction", "delta": round(delta, 4),
+                   "osk_budget": round(b2_target, 5),
+                   "select": ("fraction" if args.select == "fraction" else f"top_p {args.p}"),
+                   "delta": round(delta, 4),
                    "kv_layout": (f"paged, page {args.page_size}" if args.page_size
                                  else "contiguous"),
                    "parallelism": "single GPU"},
@@ -781,9 +840,13 @@ def main():
                      "frac": round(osk_tflops / PEAK_BF16_TFLOPS, 4), "traffic": traffic},
         "kap_score_roofline": {"hbm_gbs": round(kb / (t_score * 1e-3) / 1e9, 1),
                                "hbm_frac": round(kb / (t_score * 1e-3) / 1e9 / PEAK_HBM_GBS, 4),
+                               "hbm_gbs_counters": (round(kap_traffic / (t_score * 1e-3) / 1e9, 1)
+                                                    if kap_traffic else None),
+                               "traffic_counters": kap_traffic,
                                "mfma_tflops": round(kf / (t_score * 1e-3) / 1e12, 1),
                                "mfma_frac": round(kf / (t_score * 1e-3) / 1e12 / PEAK_BF16_TFLOPS,
                                                   4)},
+        "hbm_copy_gbs": round(copy_gbs, 1),
         "mfma_ceiling": ceiling,
         "cpu_baseline": cpu,
     }
