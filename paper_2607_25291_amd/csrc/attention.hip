@@ -109,14 +109,14 @@ __device__ __forceinline__ void copy_page(__amdgpu_buffer_rsrc_t rs, char* dst, 
 // Paged variant (Sec. 4.3 "Physical jumping over pages"): the block's rows live in physical pages of
 // 2^log2p >= 16 tokens of a [n_pages, Hkv, page, d] cache. Wave w moves the consecutive chunks
 // w * CPW .. w * CPW + CPW - 1 in runs of four (16 rows): a run starts 16-aligned, so it lies inside
-// one physical page whatever the page size, and each run takes one page lookup and one buffer
-// resource, its chunks immediate offsets from it (no per-chunk test for a page boundary). Lane k of
-// `tbl` holds the physical page of the block's k-th page-sized segment (segment 0 when a page holds
-// the block). Addressing stays 64-bit for caches of any size.
-template <int BLOCK, int NW, bool IS_K>
-__device__ __forceinline__ void copy_page_paged(const uint16_t* cache, long long page_elems,
-                                                int tbl, int first_row, int log2p, char* dst,
-                                                int w, int lane) {
+// one physical page whatever the page size, and each run takes one buffer resource, its chunks
+// immediate offsets from it (no per-chunk test for a page boundary). Lane k of `seg_lo`/`seg_hi`
+// holds the 64-bit byte address of the block's k-th page-sized segment (segment 0 when a page holds
+// the block), formed in vector registers before the copy, so that a run costs two lane reads and a
+// 64-bit add in scalar registers instead of a 64-bit multiply.
+template <int BLOCK, int NW, bool IS_K, bool WHOLE>
+__device__ __forceinline__ void copy_page_paged(int seg_lo, int seg_hi, int first_row, int log2p,
+                                                char* dst, int w, int lane) {
   constexpr int kChunks = BLOCK * kHeadDim * 2 / 1024;
   constexpr int CPW = kChunks / NW;
   static_assert(kChunks % NW == 0 && CPW % 4 == 0, "each wave moves a multiple of 16 rows");
@@ -124,14 +124,41 @@ __device__ __forceinline__ void copy_page_paged(const uint16_t* cache, long long
   // Opaque wave index: the per-chunk offsets are formed here instead of being hoisted out of the
   // page loop into scalar registers.
   asm volatile("" : "+s"(w));
+  if constexpr (WHOLE) {
+    // The block lies inside one physical page (page size >= block): one resource for the wave's
+    // chunks, as for a contiguous cache.
+    const uint64_t base = ((uint64_t)(uint32_t)__builtin_amdgcn_readfirstlane(seg_hi) << 32) |
+                          (uint32_t)__builtin_amdgcn_readfirstlane(seg_lo);
+    const int in_page = first_row & page_mask;
+    const __amdgpu_buffer_rsrc_t rs = __builtin_amdgcn_make_buffer_rsrc(
+        (void*)(base + (uint64_t)in_page * (kHeadDim * 2)), (short)0, BLOCK * kHeadDim * 2,
+        0x00020000);
+    int lds0 = (int)(size_t)COSA_LDS(dst) + w * CPW * 1024;
+    int src0 = w * CPW * 1024;
+    asm volatile("" : "+s"(lds0), "+s"(src0));
+#pragma unroll
+    for (int u = 0; u < CPW; ++u) {
+      const int row = 4 * (w * CPW + u) + (lane >> 4);
+      const int stored = lane & 15;
+      const int slot = IS_K ? (stored ^ (row & 15)) : (stored ^ ((row & 3) << 2));
+      const int voff = (lane >> 4) * (kHeadDim * 2) + slot * 16;
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(
+          rs, (__attribute__((address_space(3))) void*)(size_t)(lds0 + u * 1024), 16, voff,
+          src0 + u * 1024, 0, 0);
+    }
+    return;
+  }
 #pragma unroll
   for (int run = 0; run < CPW / 4; ++run) {
     const int row0 = (w * CPW + 4 * run) * 4;  // first row of the run within the block
     const int in_page = (first_row + row0) & page_mask;
-    const long long phys = __builtin_amdgcn_readlane(tbl, row0 >> log2p);
-    const uint16_t* base = cache + phys * page_elems + (long long)in_page * kHeadDim;
-    const __amdgpu_buffer_rsrc_t rs =
-        __builtin_amdgcn_make_buffer_rsrc((void*)base, (short)0, 16 * kHeadDim * 2, 0x00020000);
+    const int seg = row0 >> log2p;
+    const uint64_t base =
+        ((uint64_t)(uint32_t)__builtin_amdgcn_readlane(seg_hi, seg) << 32) |
+        (uint32_t)__builtin_amdgcn_readlane(seg_lo, seg);
+    const __amdgpu_buffer_rsrc_t rs = __builtin_amdgcn_make_buffer_rsrc(
+        (void*)(base + (uint64_t)in_page * (kHeadDim * 2)), (short)0, 16 * kHeadDim * 2,
+        0x00020000);
 #pragma unroll
     for (int u4 = 0; u4 < 4; ++u4) {
       const int u = 4 * run + u4;
@@ -145,6 +172,12 @@ __device__ __forceinline__ void copy_page_paged(const uint16_t* cache, long long
   }
 }
 
+// Where the keys and values live: contiguous [B, Hkv, L, d], or a paged cache whose pages are
+// smaller than a block (a block spans several pages) or at least a block (one page holds it).
+constexpr int kPgNone = 0;
+constexpr int kPgSplit = 1;
+constexpr int kPgWhole = 2;
+
 // How the key blocks of a query block are walked.
 constexpr int kWalkDense = 0;  // j = 0 .. i ascending, every block computed
 constexpr int kWalkList = 1;   // OSK: the KAP list in list order, rowmax skip vote
@@ -155,13 +188,14 @@ __global__ void queue_reset(uint32_t* queue) {
   if (threadIdx.x < kNumXcd) queue[threadIdx.x * 32] = 0u;
 }
 
-template <int BLOCK, int HPW, int WALK, bool PAGED, bool PERSIST>
+template <int BLOCK, int HPW, int WALK, int PG, bool PERSIST>
 __global__ __attribute__((amdgpu_flat_work_group_size(TileCfg<BLOCK, HPW>::kThreads,
                                                       TileCfg<BLOCK, HPW>::kThreads)))
 __attribute__((amdgpu_waves_per_eu(TileCfg<BLOCK, HPW>::kWavesPerEu,
                                    TileCfg<BLOCK, HPW>::kWavesPerEu)))
 void attention_kernel(const AttnParams P) {
   using Cfg = TileCfg<BLOCK, HPW>;
+  constexpr bool PAGED = PG != kPgNone;
   constexpr bool OSK = WALK == kWalkList;
   constexpr bool MASKED = WALK == kWalkMask;
   constexpr int KT = Cfg::kKeyTiles;
@@ -278,15 +312,16 @@ void attention_kernel(const AttnParams P) {
   auto page_of = [&](int raw) -> int { return listed(raw) ? raw : i; };
 
   // Physical pages of a listed block (paged caches): lane k loads the page of the block's k-th
-  // page-sized segment; entries outside [0, n_pages) read page 0.
+  // page-sized segment. The entry is checked only where it is used, a page later (entries outside
+  // [0, n_pages) read page 0): a check right after the load would wait for it.
   const int log2p = PAGED ? P.a.pg.log2_page : 0;
+  const unsigned n_pages = PAGED ? (unsigned)min(P.a.pg.n_pages, 1LL << 31) : 0u;
   auto table_of = [&](int raw) -> int {
     if constexpr (PAGED) {
       const int segs = BLOCK >> log2p;
       if (lane < (segs > 0 ? segs : 1)) {
         const int lp = ((page_of(raw) * BLOCK) >> log2p) + lane;
-        const int e = P.a.pg.table[(size_t)n * P.a.pg.pages_per_seq + lp];
-        return (e >= 0 && (long long)e < P.a.pg.n_pages) ? e : 0;
+        return P.a.pg.table[(size_t)n * P.a.pg.pages_per_seq + lp];
       }
     }
     return 0;
@@ -297,11 +332,15 @@ void attention_kernel(const AttnParams P) {
     constexpr int NW = decltype(nwc)::value;
     if constexpr (PAGED) {
       // K or V cache of KV head g; one physical page of one head is page * d elements, pages of
-      // consecutive page numbers are Hkv of those apart
-      const long long head_page = (long long)kHeadDim << log2p;
-      const uint16_t* cache = (IS_K ? P.a.k : P.a.v) + (long long)g * head_page;
-      copy_page_paged<BLOCK, NW, IS_K>(cache, head_page * P.Hkv, tbl, page_of(raw) * BLOCK, log2p,
-                                       dst, wv, lane);
+      // consecutive page numbers are Hkv of those apart. Lane k: the byte address of physical
+      // page tbl (the block's k-th segment).
+      const uint64_t head_page_bytes = (uint64_t)kHeadDim * 2 << log2p;
+      const uint64_t cache = (uint64_t)(IS_K ? P.a.k : P.a.v) + (uint64_t)g * head_page_bytes;
+      const uint32_t phys = (uint32_t)tbl < n_pages ? (uint32_t)tbl : 0u;
+      const uint64_t seg = cache + (uint64_t)phys * (head_page_bytes * (uint64_t)P.Hkv);
+      copy_page_paged<BLOCK, NW, IS_K, PG == kPgWhole>((int)(uint32_t)seg,
+                                                       (int)(uint32_t)(seg >> 32),
+                                                       page_of(raw) * BLOCK, log2p, dst, wv, lane);
     } else {
       copy_page<BLOCK, NW, IS_K>(IS_K ? krs : vrs, dst, page_of(raw) * PAGE, wv, lane);
     }
@@ -633,7 +672,7 @@ void attention_kernel(const AttnParams P) {
   }  // tiles of a persistent workgroup
 }
 
-template <int BLOCK, int HPW, int WALK, bool PAGED>
+template <int BLOCK, int HPW, int WALK, int PG>
 void launch_t(const AttnParams& P, int G, hipStream_t stream) {
   using Cfg = TileCfg<BLOCK, HPW>;
   const int slots = (P.n_units + kNumXcd - 1) / kNumXcd * kNumXcd * (G / HPW);
@@ -646,24 +685,24 @@ void launch_t(const AttnParams& P, int G, hipStream_t stream) {
           cus < 1)
         cus = 256;
       hipLaunchKernelGGL(queue_reset, dim3(1), dim3(64), 0, stream, P.a.queue);
-      hipLaunchKernelGGL((attention_kernel<BLOCK, HPW, WALK, PAGED, true>),
+      hipLaunchKernelGGL((attention_kernel<BLOCK, HPW, WALK, PG, true>),
                          dim3(cus < slots ? cus : slots), dim3(Cfg::kThreads), 0, stream, P);
       return;
     }
   }
-  hipLaunchKernelGGL((attention_kernel<BLOCK, HPW, WALK, PAGED, false>), dim3(slots),
+  hipLaunchKernelGGL((attention_kernel<BLOCK, HPW, WALK, PG, false>), dim3(slots),
                      dim3(Cfg::kThreads), 0, stream, P);
 }
 
-template <int WALK, bool PAGED>
+template <int WALK, int PG>
 void launch_shape(const Shape& sh, const AttnParams& P, hipStream_t stream) {
   const bool pair = (sh.G % 2) == 0;
   if (sh.b == 128) {
-    if (pair) launch_t<128, 2, WALK, PAGED>(P, sh.G, stream);
-    else launch_t<128, 1, WALK, PAGED>(P, sh.G, stream);
+    if (pair) launch_t<128, 2, WALK, PG>(P, sh.G, stream);
+    else launch_t<128, 1, WALK, PG>(P, sh.G, stream);
   } else {
-    if (pair) launch_t<64, 2, WALK, PAGED>(P, sh.G, stream);
-    else launch_t<64, 1, WALK, PAGED>(P, sh.G, stream);
+    if (pair) launch_t<64, 2, WALK, PG>(P, sh.G, stream);
+    else launch_t<64, 1, WALK, PG>(P, sh.G, stream);
   }
 }
 
@@ -680,10 +719,11 @@ hipError_t launch(const Shape& sh, const AttnArgs& a, hipStream_t stream) {
   P.scale = sh.scale;
   P.scale_log2 = sh.scale * 1.4426950408889634f;
   if constexpr (WALK == kWalkList) {
-    if (a.pg.table != nullptr) launch_shape<kWalkList, true>(sh, P, stream);
-    else launch_shape<kWalkList, false>(sh, P, stream);
+    if (a.pg.table == nullptr) launch_shape<kWalkList, kPgNone>(sh, P, stream);
+    else if ((1 << a.pg.log2_page) >= sh.b) launch_shape<kWalkList, kPgWhole>(sh, P, stream);
+    else launch_shape<kWalkList, kPgSplit>(sh, P, stream);
   } else {
-    launch_shape<WALK, false>(sh, P, stream);
+    launch_shape<WALK, kPgNone>(sh, P, stream);
   }
   return hipGetLastError();
 }
