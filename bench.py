@@ -65,9 +65,9 @@ def kap_score_work(B, Hq, Hkv, nb, b, s, d):
 
 
 def traffic_from_profile(kernel_tag: str, src: str, workload: str):
-    """HBM bytes per launch from a committed rocprofv3 counter summary, if it was taken on this
+    """HBM bytes per launch from a committed rocprofv3 counter summary, if one was taken on this
     workload and matches the current source."""
-    path = os.path.join(ROOT, "profiles", f"{kernel_tag}_traffic.json")
+    path = os.path.join(ROOT, "profiles", f"{kernel_tag}_traffic_{workload}.json")
     if not os.path.exists(path):
         return None
     with open(path) as f:
