@@ -284,9 +284,9 @@ cosa_status cosa_prefill(const cosa_problem* problem, const void* q, const void*
                          const cosa_select* select, const cosa_skip* skip, void* workspace,
                          size_t workspace_bytes, void* o, void* stream);
 
-/* Largest workspace cosa_prefill_noalloc can use: 96 MiB, which holds the workspace of one
- * 128K-token layer with 8 KV heads (88 MiB). */
-#define COSA_NOALLOC_SCRATCH_BYTES (96u * 1024u * 1024u)
+/* Largest workspace cosa_prefill_noalloc can use: 128 MiB, which holds the workspace of one
+ * 128K-token layer with 8 KV heads (120 MiB). */
+#define COSA_NOALLOC_SCRATCH_BYTES (128u * 1024u * 1024u)
 
 /*
  * For callers that cannot allocate device memory (code under HIP graph capture, tight serving

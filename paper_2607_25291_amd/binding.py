@@ -311,7 +311,7 @@ def cosa_prefill(problem, q, k, v, sel: CosaSelect, sk: Optional[CosaSkip], work
                               _ptr(workspace), workspace_bytes, _ptr(o), _stream(stream)))
 
 
-NOALLOC_SCRATCH_BYTES = 96 * 1024 * 1024
+NOALLOC_SCRATCH_BYTES = 128 * 1024 * 1024
 
 
 def cosa_prefill_noalloc(problem, q, k, v, sel: CosaSelect, sk: Optional[CosaSkip], o,

@@ -240,17 +240,23 @@ def test_workspace_layout():
         assert lay.order == al(lay.hrm + cells)
         assert lay.count == al(lay.order + 4 * cells)
         assert lay.keys == al(lay.count + 4 * Bt * Hkv * nb)
-        # staged sampled keys: every KV head's L / s keys in 32-key chunks of 32 x 128 bf16
-        staged = Bt * Hkv * -(-(L // (b // 8)) // 32) * 32 * 128 * 2
+        # staged sampled keys: every KV head's L / s keys in 32-key chunks of 32 x 128 bf16, then
+        # (G * spb = 32 rows per query block) the block maxima of the paired proxy kernel's second
+        # query block: [nb][32] floats for each workgroup of its persistent grid (a multiple of 8,
+        # at most 256, one item per KV head and pair of query blocks)
+        keys = Bt * Hkv * -(-(L // (b // 8)) // 32) * 32 * 128 * 2
+        grid = min(256, -(-(Bt * Hkv * -(-nb // 2)) // 8) * 8)
+        staged = al(keys) + grid * nb * 32 * 4
         assert B.cosa_kap_score_workspace_bytes(p) == staged
         # the OSK work-queue counters (one per XCD, 128 bytes apart) close the workspace
         assert lay.queue == al(lay.keys + staged)
         assert B.cosa_osk_attention_queue_bytes() == 8 * 128
         assert lay.total == al(lay.queue + 8 * 128)
         assert B.cosa_prefill_workspace_bytes(p) == lay.total
-    # 128K, 8 KV heads: 72 MiB of proxy tensors + 16 MiB of staged keys + 1 KiB of queue counters
+    # 128K, 8 KV heads: 72 MiB of proxy tensors + 16 MiB of staged keys + 32 MiB of paired-proxy
+    # block maxima + 1 KiB of queue counters
     assert (B.cosa_prefill_workspace_bytes(B.Problem(1, 32, 8, 131072))
-            == 88 * 2 ** 20 + 32 * 2 ** 10 + 1024)
+            == 120 * 2 ** 20 + 32 * 2 ** 10 + 1024)
 
 
 def test_delta_for_budget_host_helper():

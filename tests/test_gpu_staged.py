@@ -1,9 +1,11 @@
 """Staged proxy scoring: cosa_kap_score_staged must equal cosa_kap_score bit for bit.
 
 The staged path copies the sampled keys into a workspace in the order the matrix cores read them
-and scores from that copy; the arithmetic is the same, so score and HRM must be identical. The
-cases cover every samples-per-block variant (4, 8, 16, 32), one to four 32-row proxy tiles, a last
-chunk padded past the sampled keys, batch > 1, and the 128K shape of the benchmark. The oracle
+and scores from that copy; with at most 32 proxy rows per query block it also scores two query
+blocks per workgroup. The arithmetic and the summation order are the same, so score and HRM must
+be identical. The cases cover every samples-per-block variant (4, 8, 16, 32) on both kernels, one
+to four 32-row proxy tiles, a last chunk padded past the sampled keys, an odd number of query
+blocks, batch > 1, and the 128K shape of the benchmark. The oracle
 parity of the proxy itself is covered by the contiguous path's tests.
 """
 import sys
@@ -31,6 +33,10 @@ CASES = [
     (1, 4, 1, 1024, 128, 8),     # 16 samples per block, 64 rows (two tiles)
     (1, 4, 1, 1024, 128, 4),     # 32 samples per block, 128 rows (four tiles)
     (1, 2, 1, 320, 64, 16),      # 20 sampled keys: the only chunk is padded
+    (1, 1, 1, 1024, 128, 8),     # 16 samples per block, 16 rows: paired query blocks
+    (1, 2, 1, 2048, 128, 8),     # 16 samples per block, 32 rows: paired query blocks
+    (1, 1, 1, 1024, 128, 4),     # 32 samples per block, 32 rows: paired query blocks
+    (1, 4, 2, 1600, 64, 8),      # 25 query blocks: the last pair has one block
 ]
 
 

@@ -67,7 +67,7 @@ def test_noalloc_prefill_matches_prefill():
 
 def test_noalloc_rejects_oversized_problem():
     t = torch()
-    p = B.Problem(1, 32, 16, 131072, 128, 128, 16)       # 176 MiB of workspace
+    p = B.Problem(1, 32, 16, 131072, 128, 128, 16)       # 208 MiB of workspace
     assert B.cosa_prefill_workspace_bytes(p) > B.NOALLOC_SCRATCH_BYTES
     o = t.full((4,), 1234, dtype=t.int16, device="cuda")
     with pytest.raises(B.CosaError) as e:
