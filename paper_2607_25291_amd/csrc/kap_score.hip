@@ -550,16 +550,18 @@ __global__ __launch_bounds__(kScoreThreads) void kap_pair_kernel(const KapParams
           qrs, COSA_LDS_PTR(qst + r0 * kHeadDim), 16, voff + 16 * ((lane & 15) ^ (rho & 15)), 0, 0,
           0);
     }
-    fetch(nx, nx.seq(nx.npre, w), kb0);
-    fetch(nx, nx.seq(nx.npre + 1, w), kb1);
+    if (nx.nfast + nx.ntail > 0) fetch(nx, nx.seq(nx.npre, w), kb0);
+    if (nx.nfast + nx.ntail > 1) fetch(nx, nx.seq(nx.npre + 1, w), kb1);
   };
   if (item_q(0) >= Q) return;
   prefetch(item_q(0));
 
   for (int r = 0;; ++r) {
     const PairItem it = pair_plan<SPB>(P, item_q(r), w);
-    // This item's query rows: the 16 key loads issued after them may stay in flight.
-    asm volatile("s_waitcnt vmcnt(16)" ::: "memory");
+    // This item's query rows, and the prefetched key chunks (issued during the previous item's
+    // scores, so long since landed). A wait the compiler sees: the main loop's waits then start
+    // from nothing in flight.
+    __builtin_amdgcn_s_waitcnt(0x0F70);  // vmcnt(0)
     lds_barrier();
 #pragma unroll
     for (int t = 0; t < 2; ++t) {
@@ -656,13 +658,15 @@ __global__ __launch_bounds__(kScoreThreads) void kap_pair_kernel(const KapParams
         epi_fast(sq(k + t + 1), xb0, xb1);
         interleave();
       }
-      fetch(it, sq(k + nfp), kb0);
+      // Past the hot loop a fetch runs only for a chunk the wave has (outside the loop a
+      // conditional load costs nothing).
+      if (k + nfp < kend) fetch(it, sq(k + nfp), kb0);
       mma(kb1, xb0, xb1);
       epi_fast(sq(k + nfp - 2), xa0, xa1);
       interleave();
       epi_fast(sq(k + nfp - 1), xb0, xb1);
       k += nfp;
-      fetch(it, sq(k + 1), kb1);
+      if (k + 1 < kend) fetch(it, sq(k + 1), kb1);
     }
     // The rest (an odd fast chunk and the tail, a few per wave): kb0 and kb1 hold chunks k, k + 1.
     for (; k < kend; ++k) {
@@ -675,7 +679,7 @@ __global__ __launch_bounds__(kScoreThreads) void kap_pair_kernel(const KapParams
       }
 #pragma unroll
       for (int cc = 0; cc < 8; ++cc) kb0[cc] = kb1[cc];
-      fetch(it, sq(k + 2), kb1);
+      if (k + 2 < kend) fetch(it, sq(k + 2), kb1);
     }
 
     {
