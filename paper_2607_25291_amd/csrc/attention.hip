@@ -110,12 +110,15 @@ __device__ __forceinline__ void copy_page(__amdgpu_buffer_rsrc_t rs, char* dst, 
 // 2^log2p >= 16 tokens of a [n_pages, Hkv, page, d] cache. Wave w moves the consecutive chunks
 // w * CPW .. w * CPW + CPW - 1 in runs of four (16 rows): a run starts 16-aligned, so it lies inside
 // one physical page whatever the page size, and each run takes one buffer resource, its chunks
-// immediate offsets from it (no per-chunk test for a page boundary). Lane k of `seg_lo`/`seg_hi`
-// holds the 64-bit byte address of the block's k-th page-sized segment (segment 0 when a page holds
-// the block), formed in vector registers before the copy, so that a run costs two lane reads and a
-// 64-bit add in scalar registers instead of a 64-bit multiply.
+// immediate offsets from it (no per-chunk test for a page boundary). Lane k of `tbl` holds the raw
+// table entry of the block's k-th page-sized segment (segment 0 when a page holds the block). A run
+// reads its entry into a scalar register and forms the page address there (the range clamp, a
+// 64-bit multiply by the page stride `pstride` and the add to the head's cache base `cache`), so
+// that the copy adds no vector instructions to the wave that issues it; entries outside
+// [0, n_pages) read page 0.
 template <int BLOCK, int NW, bool IS_K, bool WHOLE>
-__device__ __forceinline__ void copy_page_paged(int seg_lo, int seg_hi, int first_row, int log2p,
+__device__ __forceinline__ void copy_page_paged(int tbl, uint64_t cache, uint64_t pstride,
+                                                unsigned n_pages, int first_row, int log2p,
                                                 char* dst, int w, int lane) {
   constexpr int kChunks = BLOCK * kHeadDim * 2 / 1024;
   constexpr int CPW = kChunks / NW;
@@ -127,8 +130,8 @@ __device__ __forceinline__ void copy_page_paged(int seg_lo, int seg_hi, int firs
   if constexpr (WHOLE) {
     // The block lies inside one physical page (page size >= block): one resource for the wave's
     // chunks, as for a contiguous cache.
-    const uint64_t base = ((uint64_t)(uint32_t)__builtin_amdgcn_readfirstlane(seg_hi) << 32) |
-                          (uint32_t)__builtin_amdgcn_readfirstlane(seg_lo);
+    const uint32_t e = (uint32_t)__builtin_amdgcn_readfirstlane(tbl);
+    const uint64_t base = cache + (uint64_t)(e < n_pages ? e : 0u) * pstride;
     const int in_page = first_row & page_mask;
     const __amdgpu_buffer_rsrc_t rs = __builtin_amdgcn_make_buffer_rsrc(
         (void*)(base + (uint64_t)in_page * (kHeadDim * 2)), (short)0, BLOCK * kHeadDim * 2,
@@ -138,7 +141,9 @@ __device__ __forceinline__ void copy_page_paged(int seg_lo, int seg_hi, int firs
     asm volatile("" : "+s"(lds0), "+s"(src0));
 #pragma unroll
     for (int u = 0; u < CPW; ++u) {
-      const int row = 4 * (w * CPW + u) + (lane >> 4);
+      // Row 4 (w CPW + u) + lane / 16 of the block; only its residue mod 16 enters the swizzle,
+      // and w CPW is a multiple of 4.
+      const int row = 4 * (u & 3) + (lane >> 4);
       const int stored = lane & 15;
       const int slot = IS_K ? (stored ^ (row & 15)) : (stored ^ ((row & 3) << 2));
       const int voff = (lane >> 4) * (kHeadDim * 2) + slot * 16;
@@ -153,16 +158,17 @@ __device__ __forceinline__ void copy_page_paged(int seg_lo, int seg_hi, int firs
     const int row0 = (w * CPW + 4 * run) * 4;  // first row of the run within the block
     const int in_page = (first_row + row0) & page_mask;
     const int seg = row0 >> log2p;
-    const uint64_t base =
-        ((uint64_t)(uint32_t)__builtin_amdgcn_readlane(seg_hi, seg) << 32) |
-        (uint32_t)__builtin_amdgcn_readlane(seg_lo, seg);
+    const uint32_t e = (uint32_t)__builtin_amdgcn_readlane(tbl, seg);
+    const uint64_t base = cache + (uint64_t)(e < n_pages ? e : 0u) * pstride;
     const __amdgpu_buffer_rsrc_t rs = __builtin_amdgcn_make_buffer_rsrc(
         (void*)(base + (uint64_t)in_page * (kHeadDim * 2)), (short)0, 16 * kHeadDim * 2,
         0x00020000);
 #pragma unroll
     for (int u4 = 0; u4 < 4; ++u4) {
       const int u = 4 * run + u4;
-      const int row = 4 * (w * CPW + u) + (lane >> 4);
+      // Row 4 (w CPW + u) + lane / 16 of the block; only its residue mod 16 enters the swizzle,
+      // and w CPW is a multiple of 4.
+      const int row = 4 * (u & 3) + (lane >> 4);
       const int stored = lane & 15;
       const int slot = IS_K ? (stored ^ (row & 15)) : (stored ^ ((row & 3) << 2));
       const int voff = (lane >> 4) * (kHeadDim * 2) + slot * 16;
@@ -311,18 +317,19 @@ void attention_kernel(const AttnParams P) {
   auto listed = [&](int raw) -> bool { return (unsigned)(raw - F) <= (unsigned)(i - F); };
   auto page_of = [&](int raw) -> int { return listed(raw) ? raw : i; };
 
-  // Physical pages of a listed block (paged caches): lane k loads the page of the block's k-th
-  // page-sized segment. The entry is checked only where it is used, a page later (entries outside
-  // [0, n_pages) read page 0): a check right after the load would wait for it.
+  // Physical pages of a listed block (paged caches): lane k loads the table entry of the block's k-th
+  // page-sized segment (the lanes past the block's segments load entries they do not use, those past
+  // the sequence's row read 0), through a buffer resource over the row of sequence n. The entry is
+  // checked only where it is used, a page later: a check right after the load would wait for it.
   const int log2p = PAGED ? P.a.pg.log2_page : 0;
   const unsigned n_pages = PAGED ? (unsigned)min(P.a.pg.n_pages, 1LL << 31) : 0u;
+  const __amdgpu_buffer_rsrc_t trs = __builtin_amdgcn_make_buffer_rsrc(
+      PAGED ? (void*)(P.a.pg.table + (size_t)n * P.a.pg.pages_per_seq) : nullptr, (short)0,
+      PAGED ? P.a.pg.pages_per_seq * 4 : 0, 0x00020000);
   auto table_of = [&](int raw) -> int {
     if constexpr (PAGED) {
-      const int segs = BLOCK >> log2p;
-      if (lane < (segs > 0 ? segs : 1)) {
-        const int lp = ((page_of(raw) * BLOCK) >> log2p) + lane;
-        return P.a.pg.table[(size_t)n * P.a.pg.pages_per_seq + lp];
-      }
+      const int lp = ((page_of(raw) * BLOCK) >> log2p) + lane;
+      return __builtin_amdgcn_raw_buffer_load_b32(trs, lp * 4, 0, 0);
     }
     return 0;
   };
@@ -332,15 +339,12 @@ void attention_kernel(const AttnParams P) {
     constexpr int NW = decltype(nwc)::value;
     if constexpr (PAGED) {
       // K or V cache of KV head g; one physical page of one head is page * d elements, pages of
-      // consecutive page numbers are Hkv of those apart. Lane k: the byte address of physical
-      // page tbl (the block's k-th segment).
+      // consecutive page numbers are Hkv of those apart.
       const uint64_t head_page_bytes = (uint64_t)kHeadDim * 2 << log2p;
       const uint64_t cache = (uint64_t)(IS_K ? P.a.k : P.a.v) + (uint64_t)g * head_page_bytes;
-      const uint32_t phys = (uint32_t)tbl < n_pages ? (uint32_t)tbl : 0u;
-      const uint64_t seg = cache + (uint64_t)phys * (head_page_bytes * (uint64_t)P.Hkv);
-      copy_page_paged<BLOCK, NW, IS_K, PG == kPgWhole>((int)(uint32_t)seg,
-                                                       (int)(uint32_t)(seg >> 32),
-                                                       page_of(raw) * BLOCK, log2p, dst, wv, lane);
+      copy_page_paged<BLOCK, NW, IS_K, PG == kPgWhole>(
+          tbl, cache, head_page_bytes * (uint64_t)P.Hkv, n_pages, page_of(raw) * BLOCK, log2p, dst,
+          wv, lane);
     } else {
       copy_page<BLOCK, NW, IS_K>(IS_K ? krs : vrs, dst, page_of(raw) * PAGE, wv, lane);
     }
