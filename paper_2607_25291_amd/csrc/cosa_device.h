@@ -56,10 +56,13 @@ __device__ __forceinline__ float half_sum(float v) {
   return lo + hi;
 }
 
+// Lane permutation within rows of 16 (every lane's source lane exists for the patterns used here,
+// so the bound-control zero fill never applies; with it the compiler can fold the move into the
+// arithmetic instruction that consumes it).
 template <int CTRL>
 __device__ __forceinline__ float dpp_mov(float v) {
   const int u = __builtin_bit_cast(int, v);
-  const int r = __builtin_amdgcn_update_dpp(u, u, CTRL, 0xF, 0xF, false);
+  const int r = __builtin_amdgcn_mov_dpp(u, CTRL, 0xF, 0xF, true);
   return __builtin_bit_cast(float, r);
 }
 

@@ -32,6 +32,7 @@ namespace {
 constexpr int kScoreThreads = 512;
 constexpr int kScoreWaves = kScoreThreads / 64;
 constexpr int kPairMaxWorkgroups = 256;  // persistent grid of kap_pair_kernel (one per CU)
+constexpr int kBDepth = 8;  // kap_pair_kernel: passes of unit B's read-back in flight
 
 struct KapParams {
   KapScoreArgs a;
@@ -344,9 +345,9 @@ __device__ __forceinline__ float group8_tree_sum(float g) {
   return g;
 }
 __device__ __forceinline__ int group8_or(int f) {
-  f |= __builtin_amdgcn_update_dpp(f, f, 0xB1, 0xF, 0xF, false);
-  f |= __builtin_amdgcn_update_dpp(f, f, 0x4E, 0xF, 0xF, false);
-  f |= __builtin_amdgcn_update_dpp(f, f, 0x141, 0xF, 0xF, false);
+  f |= __builtin_amdgcn_mov_dpp(f, 0xB1, 0xF, 0xF, true);
+  f |= __builtin_amdgcn_mov_dpp(f, 0x4E, 0xF, 0xF, true);
+  f |= __builtin_amdgcn_mov_dpp(f, 0x141, 0xF, 0xF, true);
   return f;
 }
 
@@ -541,14 +542,20 @@ __global__ __launch_bounds__(kScoreThreads) void kap_pair_kernel(const KapParams
         P.G * P.L * kHeadDim * 2, 0x00020000);
 #pragma unroll
     for (int u = 0; u < 2; ++u) {
+      // Rows rho = r0 + lane / 16 of tile t = r0 / 32: row l = lb + lane / 16 of the tile, with lb
+      // a multiple of 4 and so is SPB; hence l / SPB = lb / SPB, l % SPB = lb % SPB + lane / 16,
+      // and l < R exactly when lb < R (R a multiple of 4). All but the lane term are wave-uniform
+      // (formed in scalar registers, nothing held in vector registers across the item).
       const int r0 = 8 * w + 4 * u;  // first of the four rows
-      const int rho = r0 + (lane >> 4), t = rho >> 5, l = rho & 31;
+      const int t = r0 >> 5, lb = r0 & 31, lr = lane >> 4;
       const int iu = t ? nx.iB : nx.iA;
-      const bool real = l < P.R && (t == 0 || nx.hasB);
-      const int voff = real ? ((l / SPB) * P.L + (iu * SPB + l % SPB) * P.s) * (kHeadDim * 2) : 0;
-      __builtin_amdgcn_raw_ptr_buffer_load_lds(
-          qrs, COSA_LDS_PTR(qst + r0 * kHeadDim), 16, voff + 16 * ((lane & 15) ^ (rho & 15)), 0, 0,
-          0);
+      const bool real = lb < P.R && (t == 0 || nx.hasB);
+      const int sbase =
+          real ? ((lb / SPB) * P.L + (iu * SPB + lb % SPB) * P.s) * (kHeadDim * 2) : 0;
+      const int voff = sbase + (real ? lr * P.s * (kHeadDim * 2) : 0) +
+                       16 * ((lane & 15) ^ ((lb + lr) & 15));
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(qrs, COSA_LDS_PTR(qst + r0 * kHeadDim), 16, voff, 0,
+                                               0, 0);
     }
     if (nx.nfast + nx.ntail > 0) fetch(nx, nx.seq(nx.npre, w), kb0);
     if (nx.nfast + nx.ntail > 1) fetch(nx, nx.seq(nx.npre + 1, w), kb1);
@@ -692,22 +699,27 @@ __global__ __launch_bounds__(kScoreThreads) void kap_pair_kernel(const KapParams
     __syncthreads();  // also orders the scratch stores of every wave before the reads below
 
     // Unit B's block maxima, read back in passes of 64 key blocks: lane group tid / 8 takes block
-    // FB + tid / 8 + 64 pass, lane p = tid % 8 its rows 4p .. 4p + 3 (8 lanes read one block's 128
-    // bytes, a wave 1 KiB). The first 8 passes (512 blocks) load here, each later one while the
-    // pass 8 before it is formed. Blocks past nb - 1 read 0 (buffer range check); blocks past iB
-    // are not used.
+    // FB + tid / 8 + 64 m in pass m, lane p = tid % 8 its rows 4p .. 4p + 3 (8 lanes read one
+    // block's 128 bytes, a wave 1 KiB). The first 8 passes load here, each later one after the pass
+    // 8 before it is formed, into the registers that pass has just read (no register copy, which
+    // would wait for the load). Every load and store is unconditional, in whole rounds of 8 passes,
+    // so that the compiler's waits count exactly: a pass past the last repeats its load, and a
+    // store that must not happen (a lane other than p = 0, a block past iB, a padding pass) gets an
+    // offset past the end of its row's buffer resource, which drops it. Blocks past nb - 1 read 0
+    // (range check). Unit B's scores come before the next item's prefetch and unit A's scores, so
+    // that no load but these is in flight while they form.
     const int p8 = tid & 7, jb0 = FB + (tid >> 3);
-    const int npass = hasB ? (iB - FB + 64) >> 6 : 0;
+    // Without unit B (the last item of an odd nb) one pass runs with every store dropped.
+    const int npass = hasB ? (iB - FB + 64) >> 6 : 1;
     const __amdgpu_buffer_rsrc_t brs =
         __builtin_amdgcn_make_buffer_rsrc((void*)bB, (short)0, P.nb * 32 * 4, 0x00020000);
     const int bvoff = jb0 * 128 + 16 * p8;
     auto bload = [&](int m) __attribute__((always_inline)) -> u32x4_t {
-      return __builtin_amdgcn_raw_buffer_load_b128(brs, bvoff + 8192 * m, 0, 0);
+      return __builtin_amdgcn_raw_buffer_load_b128(brs, bvoff + 8192 * min(m, npass - 1), 0, 0);
     };
-    u32x4_t bv[8];
+    u32x4_t bv[kBDepth];
 #pragma unroll
-    for (int m = 0; m < 8; ++m)
-      if (m < npass) bv[m] = bload(m);
+    for (int m = 0; m < kBDepth; ++m) bv[m] = bload(m);
     if (tid < 64 && (tid & 31) < P.R) {
       const int t = tid >> 5, row = tid & 31;
       float v = wmax[0][t][row];
@@ -716,25 +728,24 @@ __global__ __launch_bounds__(kScoreThreads) void kap_pair_kernel(const KapParams
       (t ? muB : muA)[row] = v;
     }
     lds_barrier();
-    // The next item: its query tiles and first two key chunks load while this one's scores form.
-    const bool more = item_q(r + 1) < Q;
-    if (more) prefetch(item_q(r + 1));
 
-    float* srow = P.a.score + ((size_t)it.ng * P.nb + iA) * P.nb;
-    uint8_t* hrow = P.a.hrm + ((size_t)it.ng * P.nb + iA) * P.nb;
-    for (int j = FA + tid; j <= iA; j += kScoreThreads)
-      score_column(P.R, muA, [&](int row, float (&b)[4]) {
-#pragma unroll
-        for (int r2 = 0; r2 < 4; ++r2) b[r2] = beta[(row + r2) * P.nbp + j];
-      }, srow[j], hrow[j]);
-    if (hasB) {
-      srow -= P.nb;
-      hrow -= P.nb;
+    float* const srow = P.a.score + ((size_t)it.ng * P.nb + iA) * P.nb;
+    uint8_t* const hrow = P.a.hrm + ((size_t)it.ng * P.nb + iA) * P.nb;
+    {
+      // The lane's rows are formed afresh here (an opaque copy of the lane index): a value kept from
+      // the item's start would be spilled, and its reload would wait for every load in flight.
+      int p8o = tid & 7;
+      asm volatile("" : "+v"(p8o));
       float mb[4];
 #pragma unroll
-      for (int r2 = 0; r2 < 4; ++r2) mb[r2] = muB[(4 * p8 + r2) & 31];
+      for (int r2 = 0; r2 < 4; ++r2) mb[r2] = muB[4 * p8o + r2];
+      // Unit B's output row (query block iB, the row before unit A's): its blocks 0 .. iB.
+      const int nB = hasB ? iB + 1 : 0;
+      const __amdgpu_buffer_rsrc_t sB = __builtin_amdgcn_make_buffer_rsrc(
+          (void*)(hasB ? srow - P.nb : srow), (short)0, nB * 4, 0x00020000);
+      const __amdgpu_buffer_rsrc_t hB = __builtin_amdgcn_make_buffer_rsrc(
+          (void*)(hasB ? hrow - P.nb : hrow), (short)0, nB, 0x00020000);
       auto pass = [&](int m, const u32x4_t& v) __attribute__((always_inline)) {
-        const int j = jb0 + 64 * m;
         float b[4];
 #pragma unroll
         for (int r2 = 0; r2 < 4; ++r2) b[r2] = __builtin_bit_cast(float, (uint32_t)v[r2]);
@@ -743,26 +754,37 @@ __global__ __launch_bounds__(kScoreThreads) void kap_pair_kernel(const KapParams
         fl = 4 * p8 < P.R ? fl : 0;
         g = group8_tree_sum(g);
         fl = group8_or(fl);
-        if (p8 == 0 && j <= iB) {
-          srow[j] = g;
-          hrow[j] = (uint8_t)fl;
-        }
+        const int jo = (p8 == 0 && m < npass) ? jb0 + 64 * m : (1 << 28);  // else dropped
+        __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(uint32_t, g), sB, jo * 4, 0, 0);
+        __builtin_amdgcn_raw_buffer_store_b8((uint8_t)fl, hB, jo, 0, 0);
       };
-      for (int m0 = 0; m0 < npass; m0 += 8) {
+      const int m_last = (npass - 1) / kBDepth * kBDepth;  // first pass of the last round
+      for (int m0 = 0; m0 < m_last; m0 += kBDepth) {
 #pragma unroll
-        for (int mm = 0; mm < 8; ++mm) {
-          const int m = m0 + mm;
-          if (m < npass) {
-            const u32x4_t v = bv[mm];
-            if (m + 8 < npass) bv[mm] = bload(m + 8);
-            pass(m, v);
-          }
+        for (int mm = 0; mm < kBDepth; ++mm) {
+          pass(m0 + mm, bv[mm]);
+          __builtin_amdgcn_sched_barrier(0);
+          bv[mm] = bload(m0 + mm + kBDepth);
         }
       }
+#pragma unroll
+      for (int mm = 0; mm < kBDepth; ++mm) pass(m_last + mm, bv[mm]);
     }
+
+    // The next item: its query tiles and first two key chunks load while unit A's scores form.
+    // After the last item the current one is fetched again (nothing reads it): an unconditional
+    // prefetch loads straight into the registers the next item's loop reads, with no copy.
+    const bool more = item_q(r + 1) < Q;
+    prefetch(item_q(more ? r + 1 : r));
+    for (int j = FA + tid; j <= iA; j += kScoreThreads)
+      score_column(P.R, muA, [&](int row, float (&b)[4]) {
+#pragma unroll
+        for (int r2 = 0; r2 < 4; ++r2) b[r2] = beta[(row + r2) * P.nbp + j];
+      }, srow[j], hrow[j]);
     lds_barrier();  // beta and the row maxima are reused by the next item
     if (!more) break;
   }
+  __builtin_amdgcn_s_waitcnt(0x0F70);  // the last (unused) prefetch has landed
 }
 
 // Dynamic LDS above the default limit has to be allowed per kernel; remember the largest size
