@@ -26,7 +26,10 @@ def say(*a):
 
 
 SMALL_GQA = Workload("small_gqa", 2, 8, 2, 2048, 128, 128, 16, 0.25, 0.125, 256, (0.005, 0.03))
-CASES = {"tiny_l2k": (WORKLOADS["tiny_l2k"], [16, 64, 256]), "small_gqa": (SMALL_GQA, [16, 128, 512])}
+# Page sizes below, at and above the block size, and one page holding a whole sequence (the block's
+# rows then sit deep inside their page).
+CASES = {"tiny_l2k": (WORKLOADS["tiny_l2k"], [16, 64, 256, 2048]),
+         "small_gqa": (SMALL_GQA, [16, 128, 512, 2048])}
 
 
 def make_paged(k, v, page, extra, seed):
