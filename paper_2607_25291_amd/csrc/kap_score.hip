@@ -15,7 +15,7 @@
 //   - kap_pair_kernel (staged keys, R <= 32): a persistent workgroup per CU takes two adjacent
 //     query blocks of one KV head at a time, so that every key fragment loaded into registers
 //     feeds two MFMA tiles (64 rows). The first unit's block maxima live in LDS, the second's in a
-//     per-workgroup scratch in global memory (write-once, read-once, cache-resident).
+//     per-workgroup scratch in global memory (written and read once per item).
 //   - kap_score_kernel (every other case): one workgroup per unit, block maxima in LDS.
 // Both place work so that each XCD serves as few KV heads as possible (their sampled keys then stay
 // in that XCD's L2), heaviest query blocks first.
@@ -493,7 +493,7 @@ __device__ __forceinline__ void lds_barrier() {
 // A persistent grid of G workgroups (a multiple of 8) walks the items: in round r workgroup
 // b = 8c + x takes item q = r*G + 8c' + x with c' = c in even rounds and G/8 - 1 - c in odd ones
 // (snake order, so that heavy and light items even out), on the XCD x the item's head maps to.
-// While an item's scores are formed, the next item's query tiles and first two key chunks load.
+// While unit A's scores are formed, the next item's query tiles and first two key chunks load.
 template <int SPB>
 __global__ __launch_bounds__(kScoreThreads) void kap_pair_kernel(const KapParams P) {
   extern __shared__ float beta[];  // unit A: [32][nbp] (rows >= R unused)
