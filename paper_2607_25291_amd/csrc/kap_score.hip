@@ -298,22 +298,28 @@ __device__ __forceinline__ void load_query_tile(const KapParams& P, int ng, int 
 // Summation order of a key block's score over its rows (fixed, so that every kernel gives the
 // same bits): rows in groups of 4 summed in order, (((e0 + e1) + e2) + e3); the 8 groups of each
 // 32 rows as the tree ((g0 + g1) + (g2 + g3)) + ((g4 + g5) + (g6 + g7)), absent groups 0; the
-// 32-row blocks in order. e = exp(beta - mu) (hardware exp2 of the scaled argument, relative error
-// ~1e-7).
-__device__ __forceinline__ float group4(const float (&b)[4], const float (&mr)[4], int& fl) {
-  float s = __expf(b[0] - mr[0]);
+// 32-row blocks in order. e = exp(beta - mu) is the hardware exp2 of beta * log2(e) - mu2, one
+// fused multiply-add, with mu2 = mu * log2(e) formed once per row: the argument's rounding error
+// is relative to |beta| (about 1e-7 of it, a relative error of e below 1e-5 at the logit ranges
+// of attention), and a row's maximum gives e = 1 to within that error. The HRM flag compares beta
+// with mu itself, exactly.
+constexpr float kLog2e = 1.44269504088896341f;
+__device__ __forceinline__ float exp_arg(float b, float m2) { return fmaf(b, kLog2e, -m2); }
+__device__ __forceinline__ float group4(const float (&b)[4], const float (&mr)[4],
+                                        const float (&mr2)[4], int& fl) {
+  float s = __builtin_amdgcn_exp2f(exp_arg(b[0], mr2[0]));
 #pragma unroll
-  for (int r = 1; r < 4; ++r) s += __expf(b[r] - mr[r]);
+  for (int r = 1; r < 4; ++r) s += __builtin_amdgcn_exp2f(exp_arg(b[r], mr2[r]));
 #pragma unroll
   for (int r = 0; r < 4; ++r) fl |= (b[r] == mr[r]);
   return s;
 }
 
 // Score and HRM flag of key block j from its R block maxima (`beta(row, b)` fills rows row ..
-// row + 3) and the row maxima mu.
+// row + 3), the row maxima mu and mu2 = mu * log2(e).
 template <class Beta>
-__device__ __forceinline__ void score_column(int R, const float* mu, Beta&& beta, float& score,
-                                             uint8_t& flag) {
+__device__ __forceinline__ void score_column(int R, const float* mu, const float* mu2,
+                                             Beta&& beta, float& score, uint8_t& flag) {
   float acc = 0.f;
   int fl = 0;
   for (int rb = 0; rb < R; rb += 32) {  // R = G * spb is a multiple of 4
@@ -323,11 +329,14 @@ __device__ __forceinline__ void score_column(int R, const float* mu, Beta&& beta
       const int row = rb + 4 * p;
       g[p] = 0.f;
       if (row < R) {
-        float b[4], mr[4];
+        float b[4], mr[4], mr2[4];
         beta(row, b);
 #pragma unroll
-        for (int r = 0; r < 4; ++r) mr[r] = mu[row + r];
-        g[p] = group4(b, mr, fl);
+        for (int r = 0; r < 4; ++r) {
+          mr[r] = mu[row + r];
+          mr2[r] = mu2[row + r];
+        }
+        g[p] = group4(b, mr, mr2, fl);
       }
     }
     acc += ((g[0] + g[1]) + (g[2] + g[3])) + ((g[4] + g[5]) + (g[6] + g[7]));
@@ -355,7 +364,7 @@ __device__ __forceinline__ int group8_or(int f) {
 template <int SPB, int RT, bool PAGED, bool STAGED>
 __global__ __launch_bounds__(kScoreThreads) void kap_score_kernel(const KapParams P) {
   extern __shared__ float beta[];  // [R][nbp]
-  __shared__ float mu[RT * 32];
+  __shared__ float mu[RT * 32], mu2[RT * 32];
   __shared__ float wmax[kScoreWaves][RT * 32];  // each wave's row maxima
 
   int ng, i;
@@ -406,13 +415,14 @@ __global__ __launch_bounds__(kScoreThreads) void kap_score_kernel(const KapParam
 #pragma unroll
     for (int x = 1; x < kScoreWaves; ++x) v = fmaxf(v, wmax[x][tid]);
     mu[tid] = v;
+    mu2[tid] = v * kLog2e;
   }
   __syncthreads();
 
   float* srow = P.a.score + ((size_t)ng * P.nb + i) * P.nb;
   uint8_t* hrow = P.a.hrm + ((size_t)ng * P.nb + i) * P.nb;
   for (int j = F + tid; j <= i; j += kScoreThreads)
-    score_column(P.R, mu, [&](int row, float (&b)[4]) {
+    score_column(P.R, mu, mu2, [&](int row, float (&b)[4]) {
 #pragma unroll
       for (int r = 0; r < 4; ++r) b[r] = beta[(row + r) * P.nbp + j];
     }, srow[j], hrow[j]);
@@ -497,7 +507,7 @@ __device__ __forceinline__ void lds_barrier() {
 template <int SPB>
 __global__ __launch_bounds__(kScoreThreads) void kap_pair_kernel(const KapParams P) {
   extern __shared__ float beta[];  // unit A: [32][nbp] (rows >= R unused)
-  __shared__ float muA[32], muB[32];
+  __shared__ float muA[32], muB[32], muA2[32], muB2[32];
   __shared__ float wmax[kScoreWaves][2][32];
   // The item's query rows, [64][256 B] (tile t, row l at 32 t + l), 16-byte slot s of row rho
   // stored at slot s ^ (rho % 16) so that the operand reads hit 16 different slots. Loaded once per
@@ -726,6 +736,7 @@ __global__ __launch_bounds__(kScoreThreads) void kap_pair_kernel(const KapParams
 #pragma unroll
       for (int x = 1; x < kScoreWaves; ++x) v = fmaxf(v, wmax[x][t][row]);
       (t ? muB : muA)[row] = v;
+      (t ? muB2 : muA2)[row] = v * kLog2e;
     }
     lds_barrier();
 
@@ -736,9 +747,12 @@ __global__ __launch_bounds__(kScoreThreads) void kap_pair_kernel(const KapParams
       // the item's start would be spilled, and its reload would wait for every load in flight.
       int p8o = tid & 7;
       asm volatile("" : "+v"(p8o));
-      float mb[4];
+      float mb[4], mb2[4];
 #pragma unroll
-      for (int r2 = 0; r2 < 4; ++r2) mb[r2] = muB[4 * p8o + r2];
+      for (int r2 = 0; r2 < 4; ++r2) {
+        mb[r2] = muB[4 * p8o + r2];
+        mb2[r2] = muB2[4 * p8o + r2];
+      }
       // Unit B's output row (query block iB, the row before unit A's): its blocks 0 .. iB.
       const int nB = hasB ? iB + 1 : 0;
       const __amdgpu_buffer_rsrc_t sB = __builtin_amdgcn_make_buffer_rsrc(
@@ -749,9 +763,12 @@ __global__ __launch_bounds__(kScoreThreads) void kap_pair_kernel(const KapParams
         float b[4];
 #pragma unroll
         for (int r2 = 0; r2 < 4; ++r2) b[r2] = __builtin_bit_cast(float, (uint32_t)v[r2]);
+        // Formed on every lane and selected (rows past R hold stale values): no branch.
         int fl = 0;
-        float g = 4 * p8 < P.R ? group4(b, mb, fl) : 0.f;
-        fl = 4 * p8 < P.R ? fl : 0;
+        float g = group4(b, mb, mb2, fl);
+        const bool rows_ok = 4 * p8 < P.R;
+        g = rows_ok ? g : 0.f;
+        fl = rows_ok ? fl : 0;
         g = group8_tree_sum(g);
         fl = group8_or(fl);
         const int jo = (p8 == 0 && m < npass) ? jb0 + 64 * m : (1 << 28);  // else dropped
@@ -777,7 +794,7 @@ __global__ __launch_bounds__(kScoreThreads) void kap_pair_kernel(const KapParams
     const bool more = item_q(r + 1) < Q;
     prefetch(item_q(more ? r + 1 : r));
     for (int j = FA + tid; j <= iA; j += kScoreThreads)
-      score_column(P.R, muA, [&](int row, float (&b)[4]) {
+      score_column(P.R, muA, muA2, [&](int row, float (&b)[4]) {
 #pragma unroll
         for (int r2 = 0; r2 < 4; ++r2) b[r2] = beta[(row + r2) * P.nbp + j];
       }, srow[j], hrow[j]);
@@ -848,9 +865,9 @@ size_t stage_keys_bytes(const Shape& sh) {
 size_t pair_lds_bytes(const Shape& sh) { return (size_t)32 * (sh.nb + 1) * sizeof(float); }
 
 bool pair_applies(const Shape& sh) {
-  // Static LDS: 2.25 KiB of row maxima and 16 KiB of query rows. The query rows of one head group
-  // are addressed by 32-bit offsets.
-  return sh.G * sh.spb <= 32 && pair_lds_bytes(sh) + 18688 <= 160 * 1024 &&
+  // Static LDS: 2.5 KiB of row maxima (per wave, per row and scaled) and 16 KiB of query rows.
+  // The query rows of one head group are addressed by 32-bit offsets.
+  return sh.G * sh.spb <= 32 && pair_lds_bytes(sh) + 18944 <= 160 * 1024 &&
          (size_t)sh.G * sh.L * kHeadDim * 2 < ((size_t)1 << 31);
 }
 
@@ -891,8 +908,9 @@ size_t kap_score_lds_bytes(const Shape& sh) {
   if (R > 128) return 0;
   if (sh.spb != 4 && sh.spb != 8 && sh.spb != 16 && sh.spb != 32) return 0;
   const size_t bytes = (size_t)R * (sh.nb + 1) * sizeof(float);
-  // LDS per workgroup on gfx950 is 160 KiB; the static part (row maxima) needs at most 4.5 KiB.
-  if (bytes + 4608 > 160 * 1024) return 0;
+  // LDS per workgroup on gfx950 is 160 KiB; the static part (row maxima, per wave and per row,
+  // and scaled) needs at most 5 KiB.
+  if (bytes + 5120 > 160 * 1024) return 0;
   return bytes;
 }
 
