@@ -360,9 +360,19 @@ void attention_kernel(const AttnParams P) {
   const int raw2 = __builtin_amdgcn_readfirstlane(first_entry(2));
   int tbl_nxt = 0;
   if constexpr (PAGED) {
-    const int tbl0 = table_of(raw0);
+    // The first block's table entries come through scalar loads (lane k of tbl0 gets entry k), so
+    // that its copies start without waiting for the Q fragments' vector loads issued above; the
+    // next block's entries load as in the page loop.
+    const int nseg = max(BLOCK >> log2p, 1);
+    const int32_t* trow = P.a.pg.table + (size_t)n * P.a.pg.pages_per_seq +
+                          ((page_of(raw0) * BLOCK) >> log2p);
+    int tbl0 = 0;
+#pragma unroll
+    for (int kseg = 0; kseg < BLOCK / 16; ++kseg) {  // unconditional loads (clamped), issued together
+      const int e = ld_uniform(trow + min(kseg, nseg - 1));
+      tbl0 = lane == kseg ? e : tbl0;
+    }
     tbl_nxt = table_of(raw1);
-    __builtin_amdgcn_s_waitcnt(kVmcntLgkm0);
     if (cnt > 0) {
       copy_block(std::true_type{}, std::integral_constant<int, Cfg::kWaves>{}, raw0, tbl0, k_lds0, w);
       copy_block(std::false_type{}, std::integral_constant<int, Cfg::kWaves>{}, raw0, tbl0, v_lds0,
