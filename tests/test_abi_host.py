@@ -70,8 +70,11 @@ def test_problem_validation(change, status):
 
 
 def test_proxy_limits():
-    # 2 samples per block, and too many proxy rows per unit (G * spb > 128)
-    for p in [B.Problem(1, 8, 2, 1024, 128, 128, 64), B.Problem(1, 64, 2, 1024, 128, 128, 16)]:
+    # 2 samples per block, too many proxy rows per unit (G * spb > 128), and block maxima that do
+    # not fit the LDS: 32 proxy rows x (nb + 1) floats plus 5 KiB of static LDS fit 160 KiB up to
+    # nb = 1239 (the largest size, run on the GPU), not at nb = 1240
+    for p in [B.Problem(1, 8, 2, 1024, 128, 128, 64), B.Problem(1, 64, 2, 1024, 128, 128, 16),
+              B.Problem(1, 4, 1, 1240 * 128, 128, 128, 16)]:
         with pytest.raises(B.CosaError) as e:
             B.cosa_kap_score(p, 16, 16, 16, 16, stream=0)
         assert e.value.status == B.COSA_ERR_UNSUPPORTED
