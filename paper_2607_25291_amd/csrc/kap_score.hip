@@ -32,7 +32,7 @@ namespace {
 constexpr int kScoreThreads = 512;
 constexpr int kScoreWaves = kScoreThreads / 64;
 constexpr int kPairMaxWorkgroups = 256;  // persistent grid of kap_pair_kernel (one per CU)
-constexpr int kBDepth = 8;  // kap_pair_kernel: passes of unit B's read-back in flight
+constexpr int kBDepth = 4;  // kap_pair_kernel: passes of unit B's read-back in flight
 
 struct KapParams {
   KapScoreArgs a;
@@ -343,21 +343,6 @@ __device__ __forceinline__ void score_column(int R, const float* mu, const float
   }
   score = acc;
   flag = (uint8_t)fl;
-}
-
-// The same tree across the 8 lanes of a lane group (lane p holding group p, absent groups 0):
-// pairs, then quads, then the two halves; every lane of the group ends with the sum.
-__device__ __forceinline__ float group8_tree_sum(float g) {
-  g += dpp_mov<0xB1>(g);   // quad_perm [1,0,3,2]: g0 + g1
-  g += dpp_mov<0x4E>(g);   // quad_perm [2,3,0,1]: (g0 + g1) + (g2 + g3)
-  g += dpp_mov<0x141>(g);  // row_half_mirror: lane i <- 7 - i, the other quad
-  return g;
-}
-__device__ __forceinline__ int group8_or(int f) {
-  f |= __builtin_amdgcn_mov_dpp(f, 0xB1, 0xF, 0xF, true);
-  f |= __builtin_amdgcn_mov_dpp(f, 0x4E, 0xF, 0xF, true);
-  f |= __builtin_amdgcn_mov_dpp(f, 0x141, 0xF, 0xF, true);
-  return f;
 }
 
 // One unit per workgroup. STAGED: the sampled keys come from the staged copy (P.a.kstage).
@@ -708,28 +693,32 @@ __global__ __launch_bounds__(kScoreThreads) void kap_pair_kernel(const KapParams
     }
     __syncthreads();  // also orders the scratch stores of every wave before the reads below
 
-    // Unit B's block maxima, read back in passes of 64 key blocks: lane group tid / 8 takes block
-    // FB + tid / 8 + 64 m in pass m, lane p = tid % 8 its rows 4p .. 4p + 3 (8 lanes read one
-    // block's 128 bytes, a wave 1 KiB). The first 8 passes load here, each later one after the pass
-    // 8 before it is formed, into the registers that pass has just read (no register copy, which
-    // would wait for the load). Every load and store is unconditional, in whole rounds of 8 passes,
-    // so that the compiler's waits count exactly: a pass past the last repeats its load, and a
-    // store that must not happen (a lane other than p = 0, a block past iB, a padding pass) gets an
-    // offset past the end of its row's buffer resource, which drops it. Blocks past nb - 1 read 0
-    // (range check). Unit B's scores come before the next item's prefetch and unit A's scores, so
-    // that no load but these is in flight while they form.
-    const int p8 = tid & 7, jb0 = FB + (tid >> 3);
+    // Unit B's block maxima, read back in passes of 128 key blocks: lane group tid / 4 takes block
+    // FB + tid / 4 + 128 m in pass m, lane q = tid % 4 its rows 8q .. 8q + 7 (two 16-byte loads;
+    // 4 lanes read one block's 128 bytes). A lane forms the first level of the fixed tree over its
+    // two 4-row groups itself, and the other two levels come from two DPP adds. The first kBDepth
+    // passes load here, each later one after the pass kBDepth before it is formed, into the
+    // registers that pass has just read (no register copy, which would wait for the load). Every
+    // load and store is unconditional, in whole rounds, so that the compiler's waits count exactly:
+    // a pass past the last repeats its loads, and a store that must not happen (a lane other than
+    // q = 0, a block past iB, a padding pass) gets an offset past the end of its row's buffer
+    // resource, which drops it. Blocks past nb - 1 read 0 (range check). Unit B's scores come
+    // before the next item's prefetch and unit A's scores, so that no load but these is in flight
+    // while they form.
+    const int q4 = tid & 3, jb0 = FB + (tid >> 2);
     // Without unit B (the last item of an odd nb) one pass runs with every store dropped.
-    const int npass = hasB ? (iB - FB + 64) >> 6 : 1;
+    const int npass = hasB ? (iB - FB + 128) >> 7 : 1;
     const __amdgpu_buffer_rsrc_t brs =
         __builtin_amdgcn_make_buffer_rsrc((void*)bB, (short)0, P.nb * 32 * 4, 0x00020000);
-    const int bvoff = jb0 * 128 + 16 * p8;
-    auto bload = [&](int m) __attribute__((always_inline)) -> u32x4_t {
-      return __builtin_amdgcn_raw_buffer_load_b128(brs, bvoff + 8192 * min(m, npass - 1), 0, 0);
+    const int bvoff = jb0 * 128 + 32 * q4;
+    auto bload = [&](int m, u32x4_t (&v)[2]) __attribute__((always_inline)) {
+      const int o = bvoff + 16384 * min(m, npass - 1);
+      v[0] = __builtin_amdgcn_raw_buffer_load_b128(brs, o, 0, 0);
+      v[1] = __builtin_amdgcn_raw_buffer_load_b128(brs, o + 16, 0, 0);
     };
-    u32x4_t bv[kBDepth];
+    u32x4_t bv[kBDepth][2];
 #pragma unroll
-    for (int m = 0; m < kBDepth; ++m) bv[m] = bload(m);
+    for (int m = 0; m < kBDepth; ++m) bload(m, bv[m]);
     if (tid < 64 && (tid & 31) < P.R) {
       const int t = tid >> 5, row = tid & 31;
       float v = wmax[0][t][row];
@@ -745,34 +734,45 @@ __global__ __launch_bounds__(kScoreThreads) void kap_pair_kernel(const KapParams
     {
       // The lane's rows are formed afresh here (an opaque copy of the lane index): a value kept from
       // the item's start would be spilled, and its reload would wait for every load in flight.
-      int p8o = tid & 7;
-      asm volatile("" : "+v"(p8o));
-      float mb[4], mb2[4];
+      int q4o = tid & 3;
+      asm volatile("" : "+v"(q4o));
+      float mb[2][4], mb2[2][4];
 #pragma unroll
-      for (int r2 = 0; r2 < 4; ++r2) {
-        mb[r2] = muB[4 * p8o + r2];
-        mb2[r2] = muB2[4 * p8o + r2];
-      }
+      for (int h = 0; h < 2; ++h)
+#pragma unroll
+        for (int r2 = 0; r2 < 4; ++r2) {
+          mb[h][r2] = muB[8 * q4o + 4 * h + r2];
+          mb2[h][r2] = muB2[8 * q4o + 4 * h + r2];
+        }
       // Unit B's output row (query block iB, the row before unit A's): its blocks 0 .. iB.
       const int nB = hasB ? iB + 1 : 0;
       const __amdgpu_buffer_rsrc_t sB = __builtin_amdgcn_make_buffer_rsrc(
           (void*)(hasB ? srow - P.nb : srow), (short)0, nB * 4, 0x00020000);
       const __amdgpu_buffer_rsrc_t hB = __builtin_amdgcn_make_buffer_rsrc(
           (void*)(hasB ? hrow - P.nb : hrow), (short)0, nB, 0x00020000);
-      auto pass = [&](int m, const u32x4_t& v) __attribute__((always_inline)) {
-        float b[4];
-#pragma unroll
-        for (int r2 = 0; r2 < 4; ++r2) b[r2] = __builtin_bit_cast(float, (uint32_t)v[r2]);
-        // Formed on every lane and selected (rows past R hold stale values): no branch.
+      auto pass = [&](int m, const u32x4_t (&v)[2]) __attribute__((always_inline)) {
+        // Groups 2q and 2q + 1 (rows 8q .. 8q + 3, 8q + 4 .. 8q + 7), formed on every lane and
+        // selected (rows past R hold stale values, absent groups count 0): no branch.
+        float g[2];
         int fl = 0;
-        float g = group4(b, mb, mb2, fl);
-        const bool rows_ok = 4 * p8 < P.R;
-        g = rows_ok ? g : 0.f;
-        fl = rows_ok ? fl : 0;
-        g = group8_tree_sum(g);
-        fl = group8_or(fl);
-        const int jo = (p8 == 0 && m < npass) ? jb0 + 64 * m : (1 << 28);  // else dropped
-        __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(uint32_t, g), sB, jo * 4, 0, 0);
+#pragma unroll
+        for (int h = 0; h < 2; ++h) {
+          float b[4];
+#pragma unroll
+          for (int r2 = 0; r2 < 4; ++r2) b[r2] = __builtin_bit_cast(float, (uint32_t)v[h][r2]);
+          int f = 0;
+          g[h] = group4(b, mb[h], mb2[h], f);
+          const bool ok = 8 * q4 + 4 * h < P.R;
+          g[h] = ok ? g[h] : 0.f;
+          fl |= ok ? f : 0;
+        }
+        float t = g[0] + g[1];                   // (g_2q + g_2q+1)
+        t += dpp_mov<0xB1>(t);                   // quad_perm [1,0,3,2]: ((g0 + g1) + (g2 + g3)), ...
+        t += dpp_mov<0x4E>(t);                   // quad_perm [2,3,0,1]: the two halves
+        fl |= __builtin_amdgcn_mov_dpp(fl, 0xB1, 0xF, 0xF, true);
+        fl |= __builtin_amdgcn_mov_dpp(fl, 0x4E, 0xF, 0xF, true);
+        const int jo = (q4 == 0 && m < npass) ? jb0 + 128 * m : (1 << 28);  // else dropped
+        __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(uint32_t, t), sB, jo * 4, 0, 0);
         __builtin_amdgcn_raw_buffer_store_b8((uint8_t)fl, hB, jo, 0, 0);
       };
       const int m_last = (npass - 1) / kBDepth * kBDepth;  // first pass of the last round
@@ -781,7 +781,7 @@ __global__ __launch_bounds__(kScoreThreads) void kap_pair_kernel(const KapParams
         for (int mm = 0; mm < kBDepth; ++mm) {
           pass(m0 + mm, bv[mm]);
           __builtin_amdgcn_sched_barrier(0);
-          bv[mm] = bload(m0 + mm + kBDepth);
+          bload(m0 + mm + kBDepth, bv[mm]);
         }
       }
 #pragma unroll
