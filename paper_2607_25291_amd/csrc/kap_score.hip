@@ -525,10 +525,12 @@ __global__ __launch_bounds__(kScoreThreads) void kap_pair_kernel(const KapParams
   };
 
   bf16x8_t qf[2][8], kb0[8], kb1[8];
-  // Query rows and first two key chunks of item q (the plan is recomputed where it is used, which
-  // costs a few scalar instructions and keeps one plan live at a time). Wave w moves query rows
+  // Query rows and first key chunk of item q (the plan is recomputed where it is used, which costs
+  // a few scalar instructions and keeps one plan live at a time). Wave w moves query rows
   // 8w .. 8w + 7 (two 1 KiB loads of four rows); a row outside the item (>= R, or unit B absent)
-  // loads row 0 of the head group, whose products are never read.
+  // loads row 0 of the head group, whose products are never read. The key fetches are
+  // unconditional (a chunk the wave does not have loads a clamped one that is never read), so they
+  // load straight into the registers the item's loop reads, with no copy.
   auto prefetch = [&](int q) __attribute__((always_inline)) {
     const PairItem nx = pair_plan<SPB>(P, q, w);
     const int n = nx.ng / P.Hkv, g = nx.ng % P.Hkv;
@@ -552,11 +554,16 @@ __global__ __launch_bounds__(kScoreThreads) void kap_pair_kernel(const KapParams
       __builtin_amdgcn_raw_ptr_buffer_load_lds(qrs, COSA_LDS_PTR(qst + r0 * kHeadDim), 16, voff, 0,
                                                0, 0);
     }
-    if (nx.nfast + nx.ntail > 0) fetch(nx, nx.seq(nx.npre, w), kb0);
-    if (nx.nfast + nx.ntail > 1) fetch(nx, nx.seq(nx.npre + 1, w), kb1);
+    fetch(nx, nx.seq(nx.npre, w), kb0);
+  };
+  // The item's second key chunk.
+  auto prefetch_k1 = [&](int q) __attribute__((always_inline)) {
+    const PairItem nx = pair_plan<SPB>(P, q, w);
+    fetch(nx, nx.seq(nx.npre + 1, w), kb1);
   };
   if (item_q(0) >= Q) return;
   prefetch(item_q(0));
+  prefetch_k1(item_q(0));
 
   for (int r = 0;; ++r) {
     const PairItem it = pair_plan<SPB>(P, item_q(r), w);
@@ -791,13 +798,20 @@ __global__ __launch_bounds__(kScoreThreads) void kap_pair_kernel(const KapParams
     // The next item: its query tiles and first two key chunks load while unit A's scores form.
     // After the last item the current one is fetched again (nothing reads it): an unconditional
     // prefetch loads straight into the registers the next item's loop reads, with no copy.
+    // The second key chunk's loads go out after this wave's first column of unit A's scores, so
+    // that their issue overlaps that column's arithmetic instead of stalling in one burst.
     const bool more = item_q(r + 1) < Q;
-    prefetch(item_q(more ? r + 1 : r));
-    for (int j = FA + tid; j <= iA; j += kScoreThreads)
+    const int qn = item_q(more ? r + 1 : r);
+    prefetch(qn);
+    auto column_a = [&](int j) __attribute__((always_inline)) {
       score_column(P.R, muA, muA2, [&](int row, float (&b)[4]) {
 #pragma unroll
         for (int r2 = 0; r2 < 4; ++r2) b[r2] = beta[(row + r2) * P.nbp + j];
       }, srow[j], hrow[j]);
+    };
+    if (FA + tid <= iA) column_a(FA + tid);
+    prefetch_k1(qn);
+    for (int j = FA + tid + kScoreThreads; j <= iA; j += kScoreThreads) column_a(j);
     lds_barrier();  // beta and the row maxima are reused by the next item
     if (!more) break;
   }
