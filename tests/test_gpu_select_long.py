@@ -1,7 +1,9 @@
 """Stage-1 selection on long rows: nb = 1024 candidate blocks per row (the 128K benchmark at
 b = 128) and nb = 4096 (a 512K-token sequence), the row lengths where the kernel's LDS exceeds the
 default dynamic limit, the kept set outgrows one wavefront's sort and the top-p running mass covers
-hundreds of entries.
+hundreds of entries. The fraction cut runs on one wavefront per row up to 2048 candidates and on a
+workgroup per row beyond, so both kernels are covered; a second test puts the cut inside runs of
+tied scores on rows of 1 to 2048 candidates.
 
 The scores and flags are seeded random inputs fed to both sides: the HIP selection must match the
 oracle's rule (Sec. 4.2 "Flag-grouped sorting", Eq. (mkap); Algorithm A, proxy stage, top-p) bit for
@@ -65,3 +67,42 @@ def test_select_long_rows(rows, mode, value, order_mode):
     kept = [int(gc[0, 0, i]) for i in sample]
     say(f"  {len(units)} rows identical; largest kept set {max(kept)}, "
         f"kept {sum(kept)} of {sum(i + 1 for i in sample)} candidates on the sampled rows")
+
+
+@pytest.mark.parametrize("nb", [1, 40, 64, 65, 300, 2048])
+@pytest.mark.parametrize("value", [0.02, 0.10, 0.50, 1.0])
+@pytest.mark.parametrize("order_mode", [B.ORDER_KAP, B.ORDER_ASCENDING])
+def test_fraction_cut_ties_and_row_lengths(nb, value, order_mode):
+    """The fraction cut on rows whose length straddles whole wavefronts (1, 40, 64, 65, 300 and
+    2048 candidates) with heavy score ties: scores drawn from {0, a denormal, 0.5, 1, 2} plus a
+    continuous share, so the cut falls inside runs of equal scores and the block-index tie-break
+    decides. Every row (sampled rows at nb = 2048) must equal the oracle's ordering."""
+    say(f"[fraction cut ties] nb={nb} value={value} order={order_mode}")
+    rng = np.random.default_rng(7 * nb + int(value * 100) + 1000 * order_mode)
+    levels = np.array([0.0, 1e-40, 0.5, 1.0, 2.0], np.float32)
+    score = levels[rng.integers(0, len(levels), size=(1, 1, nb, nb))]
+    cont = rng.random((1, 1, nb, nb)) < 0.3
+    score = np.where(cont, rng.gamma(2.0, 1.0, size=score.shape).astype(np.float32), score)
+    hrm = (rng.random((1, 1, nb, nb)) < 0.01).astype(np.uint8)
+    t = torch()
+    p = B.Problem(1, 1, 1, nb * 128, 128, 128, 16)
+    sd = t.from_numpy(score).cuda()
+    hd = t.from_numpy(hrm).cuda()
+    order = t.full((1, 1, nb, nb), -7, dtype=t.int32, device="cuda")
+    count = t.full((1, 1, nb), -7, dtype=t.int32, device="cuda")
+    B.cosa_kap_select_ordered(p, sd, hd, B.select(B.SELECT_FRACTION, value, order_mode), order,
+                              count)
+    t.cuda.synchronize()
+    if nb <= 300:
+        sample = list(range(nb))
+    else:
+        sample = sorted(set([0, 1, 63, 64, 65, 1023, 1024, nb - 2, nb - 1] +
+                            [int(x) for x in rng.integers(0, nb, 24)]))
+    units = [(0, 0, i) for i in sample]
+    oo, oc = O.kap_select(score.astype(np.float64), hrm, mode=B.SELECT_FRACTION, value=value,
+                          order_mode=order_mode, units=units)
+    go, gc = order.cpu().numpy(), count.cpu().numpy()
+    for (n, g, i) in units:
+        assert gc[n, g, i] == oc[n, g, i], i
+        assert np.array_equal(go[n, g, i], oo[n, g, i]), i
+    say(f"  {len(units)} rows identical")
