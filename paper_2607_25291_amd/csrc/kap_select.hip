@@ -283,8 +283,7 @@ __device__ __forceinline__ uint32_t lanes_below(uint64_t b) {
 
 template <int T>
 __global__ __launch_bounds__(kWaveRows * 64) __attribute__((amdgpu_waves_per_eu(T <= 16 ? 8 : 4)))
-void kap_select_wave_kernel(const SelParams P,
-                                                                        const int k2max) {
+void kap_select_wave_kernel(const SelParams P, const int k2max) {
   extern __shared__ uint64_t wave_lds[];
   const int lane = threadIdx.x & 63;
   const int w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
