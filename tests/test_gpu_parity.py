@@ -332,6 +332,11 @@ def test_full_size_sampled(name, n_blocks_sample):
     o_pf = run.prefill(sel, sk)[0]
     assert np.array_equal(host_bits(o_pf), host_bits(o))       # prefill == its three stages
     say(f"  B1 {listed / total:.4f}  B {b_real:.4f}  delta {delta:.2f}")
+    # the selection, fed the GPU's own scores: every row bit-exact with the oracle's rule
+    oo_g, oc_g = O.kap_select(gs.astype(np.float64), gh, mode=O.SELECT_FRACTION,
+                              value=w.kap_budget)
+    assert np.array_equal(gc, oc_g) and np.array_equal(go, oo_g)
+    say(f"  selection on the GPU's scores: all {gc.size} rows bit-exact")
     kv_units, q_units = _sample_units(w, n_blocks_sample)
     # proxy on sampled KV-head units (every group the sampled query heads walk)
     say(f"  oracle KAP on {len(kv_units)} units")
